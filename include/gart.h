@@ -1,0 +1,234 @@
+/*
+ * gart.h -- C ABI of the 3DGART hot path on MI355X (gfx950).
+ *
+ * Ray-traced 3D Gaussian rendering (Sec. 3.1-3.3) with the primitive-centric
+ * backward pass (Sec. 4): conservative screen-space bounds and the
+ * intermediate-buffer pre-allocation (Sec. 4.2), the tile-primitive mapping
+ * (Sec. 4.3), a software forward trace that fills the (L, T) intermediate
+ * buffer, and a backward in which one GPU lane owns one (tile, primitive)
+ * pair (Sec. 4.4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every pointer is a DEVICE pointer unless the comment says "host".
+ *    All device memory is owned and allocated by the caller; the library
+ *    never allocates, frees or keeps device memory, and keeps no state
+ *    between calls other than what the caller's gart_frame holds.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default
+ *    stream) and is asynchronous, except for the single documented
+ *    device->host copy in gart_bounds.
+ *  - Arguments are validated before anything is launched; an invalid
+ *    argument returns GART_ERR_INVALID_ARG and launches nothing.  A failing
+ *    HIP call returns GART_ERR_HIP.  Kernels never read or write outside
+ *    the sizes the caller declares.
+ *  - One gart_frame is used by one stream at a time.  Calls on the same
+ *    frame from different streams race.
+ *  - Scene: N Gaussians with mean mu, rotation from a quaternion q = (w, x,
+ *    y, z) (any non-zero norm; normalised internally), per-axis scale
+ *    s = exp(log_scale), opacity sigma = 1 / (1 + exp(-logit)) and RGB
+ *    radiance given by real spherical harmonics of degree 0..3 evaluated at
+ *    the unit ray direction (Sec. 3.1): colour = max(0, 0.5 + sum_k
+ *    sh[k] Y_k(d)), with Y_l^m the real harmonics without Condon-Shortley
+ *    phase, k = l*l + l + m.
+ *  - Camera: pinhole, OpenCV axes, world-to-camera x_c = R x_w + t.  Pixel
+ *    (x, y) is traced through its centre (x + 0.5, y + 0.5).
+ *  - A ray hits a Gaussian iff its max-response point (Eq. 4-5) lies in
+ *    front of the camera (tau > 0) and inside the clamped ellipsoid of
+ *    radius alpha_c = sqrt(2 log(sigma / alpha_min)) (Eq. 9-10), i.e. iff
+ *    alpha = sigma rho >= alpha_min (Eq. 8).  Hits are composited front to
+ *    back in (tau, index) order (Eq. 6-7) until the transmittance falls
+ *    below t_min; the hit that crosses is included.  No cap on hits.
+ *    Background is black.
+ */
+#ifndef GART_H_
+#define GART_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GART_OK = 0,
+  GART_ERR_INVALID_ARG = -1, /* bad size, pointer, enum value or call order */
+  GART_ERR_CAPACITY = -2,    /* frame buffers too small; required sizes returned */
+  GART_ERR_HIP = -3,         /* a HIP runtime call failed */
+  GART_ERR_UNSUPPORTED = -4  /* valid but not implemented (e.g. SH degree > 3) */
+} gart_status;
+
+typedef enum {
+  GART_BACKWARD_GATHER = 0,        /* (tile, prim) pairs -> per-pair rows -> one reduction per primitive */
+  GART_BACKWARD_GATHER_ATOMIC = 1, /* (tile, prim) pairs -> one atomic update per pair (Sec. 4.4 as printed) */
+  GART_BACKWARD_SCATTER = 2        /* pixel-centric control: one atomic update per composited hit (Sec. 3.5) */
+} gart_backward_mode;
+
+/* Pinhole camera.  Host struct, passed by pointer. */
+typedef struct {
+  int32_t width, height;   /* image size in pixels, both >= 1 */
+  float fx, fy, cx, cy;    /* intrinsics in pixels; fx, fy > 0 */
+  float R[9];              /* world -> camera rotation, row-major */
+  float t[3];              /* world -> camera translation */
+} gart_camera;
+
+/* Gaussian parameters (Sec. 3.1).  Host struct holding device pointers to
+ * float32 arrays, structure-of-arrays, C-contiguous. */
+typedef struct {
+  int64_t n;                 /* number of Gaussians, 0 <= n < 2^31 */
+  int32_t sh_degree;         /* 0..3; K = (sh_degree + 1)^2 */
+  const float* means;        /* [n,3] */
+  const float* log_scales;   /* [n,3] */
+  const float* quats;        /* [n,4] (w, x, y, z) */
+  const float* opacity_logits; /* [n] */
+  const float* sh;           /* [n,K,3] */
+} gart_gaussians;
+
+typedef struct {
+  float alpha_min;        /* response cut-off, 1/255 in the paper (Sec. 3.4); in (0, 1) */
+  float t_min;            /* stop a ray once its transmittance drops below this; in (0, 1) */
+  int32_t tile;           /* tile edge in pixels: 8 or 16 (Sec. 4.4 uses 8) */
+  int32_t backward_mode;  /* gart_backward_mode */
+} gart_settings;
+
+/* Per-pixel state the forward leaves for the backward (16 bytes): the depth
+ * and index of the last composited hit if the ray terminated (T < t_min),
+ * else tau_end = +inf and id_end = 0xffffffff; a hit (tau, i) of this pixel
+ * was composited iff (tau, i) <= (tau_end, id_end) lexicographically. */
+typedef struct {
+  double tau_end;
+  uint32_t id_end;
+  uint32_t n_hits;        /* composited hits of the pixel */
+} gart_pixel_state;
+
+/* Per-frame buffers.  Host struct; the caller allocates every device array
+ * (sizes in the comments; "cap" = the capacity fields) and the library
+ * fills them.  Fields marked [out] are written by the library. */
+typedef struct {
+  /* written by gart_bounds */
+  int32_t* rect;          /* [n,4] inclusive pixel rectangle x0,y0,x1,y1; x0 > x1 if culled */
+  int64_t* lt_offset;     /* [n+1] O_prim: exclusive prefix sum of rectangle areas; [n] = total */
+  double* prim_geom;      /* [n,16] per-Gaussian fp64 precompute (opaque layout) */
+  uint32_t* tile_count;   /* [n] tiles overlapped by the rectangle */
+  /* written by gart_build_tile_map */
+  int64_t* pair_offset;   /* [n+1] first pair slot of each Gaussian in emission order */
+  int64_t pair_capacity;  /* number of (tile, prim) pair slots allocated */
+  uint32_t* pair_tile;    /* [pair_capacity] tile id of each pair, sorted ascending */
+  uint32_t* pair_prim;    /* [pair_capacity] Gaussian index of each pair */
+  int64_t* tile_range;    /* [n_tiles+1] pairs of tile t are [tile_range[t], tile_range[t+1]) */
+  /* written by gart_forward, read by gart_backward */
+  int64_t lt_capacity;    /* number of (L,T) entries allocated */
+  float* lt;              /* [lt_capacity,4] (L.r, L.g, L.b, T) in front of each composited hit */
+  gart_pixel_state* pixel_state; /* [height*width] per-pixel end marker (see gart_pixel_state) */
+  /* scratch for sorting and gradient accumulation, size from gart_scratch_bytes */
+  void* scratch;
+  size_t scratch_bytes;
+  /* optional device counters (NULL = not counted), uint64[GART_NUM_COUNTERS] */
+  uint64_t* counters;
+  /* [out] host-side totals and call-order state, filled by the library */
+  int64_t n;              /* Gaussians seen by gart_bounds */
+  int32_t sh_degree;
+  int32_t tiles_x, tiles_y;
+  int64_t lt_entries;     /* sum of rectangle areas (Eq. 15 without slack) */
+  int64_t pair_count;     /* number of (tile, prim) pairs */
+  int32_t stage;          /* 0 none, 1 bounds, 2 tile map, 3 forward */
+} gart_frame;
+
+enum {
+  GART_CNT_FWD_HITS = 0,      /* composited hits written by the forward */
+  GART_CNT_FWD_TESTS = 1,     /* (pixel, Gaussian) ray tests in the forward */
+  GART_CNT_FWD_RESCANS = 2,   /* forward rescans of a tile list (hit-buffer overflow) */
+  GART_CNT_BWD_HITS = 3,      /* composited hits visited by the backward */
+  GART_CNT_BWD_TESTS = 4,     /* (pixel, Gaussian) ray tests in the backward */
+  GART_CNT_BWD_ATOMICS = 5,   /* float atomic adds issued by the backward */
+  GART_CNT_BWD_PAIRS = 6,     /* (tile, prim) pairs visited by the backward */
+  GART_NUM_COUNTERS = 8
+};
+
+/* Bytes of scratch a frame needs for n Gaussians of the given SH degree and
+ * pair_capacity pair slots (all backward modes covered).  Pure host
+ * function. */
+size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, const gart_camera* camera,
+                          const gart_settings* settings);
+
+/* Pre-processing (Sec. 4.2, Eq. 9-15; Sec. 5.3 "pre-processing").
+ * Per Gaussian: normalised rotation, scales, opacity, clamp radius, the
+ * world-to-Gaussian map W = S^-1 R^T and o_g = W (o - mu) (Eq. 5), and the
+ * conservative pixel rectangle from the projected dual quadric
+ * T' = VPM T (Eq. 11-14).  For an ellipsoid that crosses the camera's eye
+ * plane (where Eq. 12-14 do not apply) the rectangle is the hull of the
+ * pixel columns / rows whose plane through the camera meets the ellipsoid.
+ * Culled (rect x0 > x1, area 0): sigma <= alpha_min, ellipsoid behind the
+ * camera, no pixel centre covered, non-finite parameters.
+ * Then O_prim = exclusive prefix sum of the areas (Sec. 4.3 "primitive
+ * offset").  Writes rect, lt_offset, prim_geom, tile_count and frame->n,
+ * sh_degree, tiles_x, tiles_y, lt_entries, pair_count, stage.
+ * Synchronises `stream` once to copy the two totals to the host:
+ * *lt_entries_host = sum A_i (Eq. 15 with lambda_s = 1), *pair_count_host =
+ * number of (tile, prim) pairs.  Either host pointer may be NULL.
+ * Returns GART_ERR_CAPACITY (after filling the totals) if they exceed
+ * frame->lt_capacity or frame->pair_capacity; the caller may grow the
+ * buffers (the paper's slack factor lambda_s) and call again. */
+gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                        gart_frame* frame, int64_t* lt_entries_host, int64_t* pair_count_host, void* stream);
+
+/* Tile-primitive mapping (Sec. 4.3 "reverse tile mapping").
+ * Emits one (tile, Gaussian) pair per tile that a rectangle overlaps and
+ * radix-sorts the pairs by tile id, then builds tile_range (the tile offset
+ * table).  Within one tile, pairs are ordered by a conservative lower bound
+ * on the depth at which the Gaussian can be hit (then by index); the set of
+ * Gaussians per tile is exactly the set of rectangles meeting the tile.
+ * Requires gart_bounds on the same frame first (else INVALID_ARG). */
+gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* settings, gart_frame* frame,
+                                void* stream);
+
+/* Forward trace (Sec. 3.2-3.3, Eq. 3-8; Sec. 4.3 "LT buffer access").
+ * One workgroup per tile, one lane per pixel.  Each ray tests the
+ * Gaussians of its tile list whose rectangle contains the pixel, orders the
+ * hits by (tau, index), composites them front to back and, for every
+ * composited hit of Gaussian i at pixel p in tile t, writes
+ * lt[idx(i,t,p)] = (L.rgb, T) -- the colour accumulated and the
+ * transmittance in front of the hit -- with idx(i,t,p) = O_prim(i) +
+ * O_tile(i,t) + O_pixel(i,t,p) (Eq. 16): tiles of the rectangle in
+ * row-major order, pixels row-major inside each tile.  Entries for
+ * pixels that are not composited hits are left untouched.
+ * image: [height,width,3] float32, written for every pixel.
+ * pixel_state is written for every pixel.
+ * Requires gart_build_tile_map first (else INVALID_ARG). */
+gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                         gart_frame* frame, float* image, void* stream);
+
+/* Backward (Sec. 4.4).  Gradient of L = sum_p <dL_dimage[p], C[p]> with
+ * respect to the raw parameters, OVERWRITING g_means [n,3],
+ * g_log_scales [n,3], g_quats [n,4] (w.r.t. the unnormalised input
+ * quaternion), g_logits [n] and g_sh [n,K,3].
+ * settings->backward_mode:
+ *   GATHER: one workgroup per tile; lane j owns pairs j, j+B, ... of the
+ *     tile list, walks the pixels of rect cap tile, re-tests the ray,
+ *     reads (L,T) from the intermediate buffer for composited hits and
+ *     accumulates the Gaussian's gradient in registers; each pair writes
+ *     one partial row and a per-Gaussian reduction sums its rows and
+ *     applies the chain rule.  Deterministic.
+ *   GATHER_ATOMIC: as GATHER, but each pair adds its partial into
+ *     per-Gaussian accumulators with one atomic update per value.
+ *   SCATTER: the pixel-centric control (Sec. 3.5): one lane per pixel, one
+ *     atomic add per gradient value per composited hit.
+ * image must be the forward's output for the same frame; dL_dimage is
+ * [height,width,3] float32.  Requires gart_forward first (else
+ * INVALID_ARG). */
+gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                          const gart_frame* frame, const float* image, const float* dL_dimage, float* g_means,
+                          float* g_log_scales, float* g_quats, float* g_logits, float* g_sh, void* stream);
+
+/* Human-readable name of a status code (static string). */
+const char* gart_status_string(gart_status status);
+
+/* Last error detail of the calling thread (static thread-local string;
+ * empty if none). */
+const char* gart_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GART_H_ */

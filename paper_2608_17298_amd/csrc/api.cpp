@@ -1,0 +1,367 @@
+// C ABI entry points (include/gart.h): argument validation, scratch layout
+// and the launch sequence of each step.  No device memory is allocated here.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/gart.h"
+#include "ops.h"
+
+using namespace gart;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+gart_status fail(gart_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+#define GART_HIP(expr)                                                                   \
+  do {                                                                                   \
+    const hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess) return fail(GART_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+#define GART_REQUIRE(cond, ...)                                   \
+  do {                                                            \
+    if (!(cond)) return fail(GART_ERR_INVALID_ARG, __VA_ARGS__); \
+  } while (0)
+
+size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
+
+struct Layout {
+  size_t depth_key, key_alt, perm, perm_alt, base_rank, pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals,
+      acc, rows, row_flag, total;
+};
+
+Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode) {
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  const int64_t nn = std::max<int64_t>(n, 1), pc = std::max<int64_t>(pair_cap, 1);
+  L.depth_key = take(nn * 4);
+  L.key_alt = take(nn * 4);
+  L.perm = take(nn * 4);
+  L.perm_alt = take(nn * 4);
+  L.base_rank = take((nn + 1) * 8);
+  L.pair_key_alt = take(pc * 4);
+  L.pair_val_alt = take(pc * 4);
+  L.radix_tmp = take(radix_tmp_bytes(std::max(nn, pc)));
+  L.scan_tmp = take(scan_tmp_bytes(nn + 1));
+  L.totals = take(64);
+  const size_t AS = size_t(acc_stride(K));
+  L.acc = take(mode == GART_BACKWARD_GATHER ? 4 : size_t(nn) * AS * 4);
+  L.rows = take(mode == GART_BACKWARD_GATHER ? size_t(pc) * AS * 4 : 4);
+  L.row_flag = take(mode == GART_BACKWARD_GATHER ? size_t(pc) : 4);
+  L.total = off;
+  return L;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+bool finite_f(float v) { return std::isfinite(v); }
+
+gart_status check_camera(const gart_camera* c) {
+  GART_REQUIRE(c != nullptr, "camera is NULL");
+  GART_REQUIRE(c->width >= 1 && c->height >= 1, "image size %dx%d", c->width, c->height);
+  GART_REQUIRE(int64_t(c->width) * c->height < (int64_t(1) << 31), "image too large");
+  GART_REQUIRE(finite_f(c->fx) && finite_f(c->fy) && c->fx > 0 && c->fy > 0, "focal lengths must be > 0");
+  GART_REQUIRE(finite_f(c->cx) && finite_f(c->cy), "principal point not finite");
+  for (int k = 0; k < 9; ++k) GART_REQUIRE(finite_f(c->R[k]), "camera R not finite");
+  for (int k = 0; k < 3; ++k) GART_REQUIRE(finite_f(c->t[k]), "camera t not finite");
+  return GART_OK;
+}
+
+gart_status check_settings(const gart_settings* s) {
+  GART_REQUIRE(s != nullptr, "settings is NULL");
+  GART_REQUIRE(s->alpha_min > 0.0f && s->alpha_min < 1.0f, "alpha_min must be in (0,1)");
+  GART_REQUIRE(s->t_min > 0.0f && s->t_min < 1.0f, "t_min must be in (0,1)");
+  GART_REQUIRE(s->tile == 8 || s->tile == 16, "tile must be 8 or 16");
+  GART_REQUIRE(s->backward_mode >= 0 && s->backward_mode <= 2, "unknown backward_mode %d", s->backward_mode);
+  return GART_OK;
+}
+
+gart_status check_gaussians(const gart_gaussians* g) {
+  GART_REQUIRE(g != nullptr, "gaussians is NULL");
+  GART_REQUIRE(g->n >= 0 && g->n < (int64_t(1) << 31) - 1, "n out of range");
+  if (g->sh_degree > 3) return fail(GART_ERR_UNSUPPORTED, "sh_degree %d > 3", g->sh_degree);
+  GART_REQUIRE(g->sh_degree >= 0, "sh_degree < 0");
+  if (g->n > 0)
+    GART_REQUIRE(g->means && g->log_scales && g->quats && g->opacity_logits && g->sh, "null parameter pointer");
+  return GART_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+CamParams make_cam(const gart_camera* c) {
+  CamParams p{};
+  double R[9], t[3];
+  for (int k = 0; k < 9; ++k) R[k] = c->R[k];
+  for (int k = 0; k < 3; ++k) t[k] = c->t[k];
+  for (int j = 0; j < 3; ++j)
+    for (int k = 0; k < 3; ++k) p.Rt[3 * j + k] = R[3 * k + j];
+  for (int k = 0; k < 3; ++k) p.o[k] = -(R[k] * t[0] + R[3 + k] * t[1] + R[6 + k] * t[2]);
+  p.fx = c->fx;
+  p.fy = c->fy;
+  p.cx = c->cx;
+  p.cy = c->cy;
+  for (int k = 0; k < 3; ++k) {
+    p.V0[k] = p.fx * R[k] + p.cx * R[6 + k];
+    p.V1[k] = p.fy * R[3 + k] + p.cy * R[6 + k];
+    p.V3[k] = R[6 + k];
+  }
+  p.V0[3] = p.fx * t[0] + p.cx * t[2];
+  p.V1[3] = p.fy * t[1] + p.cy * t[2];
+  p.V3[3] = t[2];
+  p.W = c->width;
+  p.H = c->height;
+  return p;
+}
+
+int tiles_along(int pixels, int tile) { return (pixels + tile - 1) / tile; }
+
+}  // namespace
+
+extern "C" {
+
+const char* gart_status_string(gart_status s) {
+  switch (s) {
+    case GART_OK: return "GART_OK";
+    case GART_ERR_INVALID_ARG: return "GART_ERR_INVALID_ARG";
+    case GART_ERR_CAPACITY: return "GART_ERR_CAPACITY";
+    case GART_ERR_HIP: return "GART_ERR_HIP";
+    case GART_ERR_UNSUPPORTED: return "GART_ERR_UNSUPPORTED";
+  }
+  return "unknown gart_status";
+}
+
+const char* gart_last_error(void) { return g_err; }
+
+size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, const gart_camera* camera,
+                          const gart_settings* settings) {
+  (void)camera;
+  const int deg = std::min(std::max(sh_degree, 0), 3);
+  const int mode = settings ? settings->backward_mode : GART_BACKWARD_GATHER;
+  return make_layout(std::max<int64_t>(n, 0), (deg + 1) * (deg + 1), std::max<int64_t>(pair_capacity, 0), mode)
+      .total;
+}
+
+gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                        gart_frame* f, int64_t* lt_entries_host, int64_t* pair_count_host, void* stream) {
+  g_err[0] = 0;
+  gart_status st;
+  if ((st = check_gaussians(g)) != GART_OK) return st;
+  if ((st = check_camera(camera)) != GART_OK) return st;
+  if ((st = check_settings(settings)) != GART_OK) return st;
+  GART_REQUIRE(f != nullptr, "frame is NULL");
+  const int64_t n = g->n;
+  const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
+  GART_REQUIRE(f->lt_offset != nullptr && f->scratch != nullptr, "frame lt_offset/scratch is NULL");
+  if (n > 0) GART_REQUIRE(f->rect && f->prim_geom && f->tile_count, "frame per-Gaussian buffer is NULL");
+  GART_REQUIRE(f->rect == nullptr || aligned16(f->rect), "rect must be 16-byte aligned");
+  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode);
+  GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  f->stage = 0;
+  unsigned long long* pair_total = at<unsigned long long>(f->scratch, L.totals);
+  GART_HIP(fill_u32(reinterpret_cast<uint32_t*>(pair_total), 0u, 2, s));
+  BoundsArgs A{};
+  A.means = g->means;
+  A.log_scales = g->log_scales;
+  A.quats = g->quats;
+  A.logits = g->opacity_logits;
+  A.n = n;
+  A.cam = make_cam(camera);
+  A.alpha_min = settings->alpha_min;
+  A.tile = settings->tile;
+  A.rect = f->rect;
+  A.area = f->lt_offset;
+  A.geom = f->prim_geom;
+  A.tile_count = f->tile_count;
+  A.depth_key = at<uint32_t>(f->scratch, L.depth_key);
+  A.pair_total = pair_total;
+  GART_HIP(launch_bounds(A, s));
+  GART_HIP(scan_exclusive_i64(f->lt_offset, f->lt_offset, n, f->lt_offset + n, at<void>(f->scratch, L.scan_tmp), s));
+  int64_t host[2] = {0, 0};
+  GART_HIP(hipMemcpyAsync(&host[0], f->lt_offset + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  GART_HIP(hipMemcpyAsync(&host[1], pair_total, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  GART_HIP(hipStreamSynchronize(s));
+
+  f->n = n;
+  f->sh_degree = g->sh_degree;
+  f->tiles_x = tiles_along(camera->width, settings->tile);
+  f->tiles_y = tiles_along(camera->height, settings->tile);
+  f->lt_entries = host[0];
+  f->pair_count = host[1];
+  if (lt_entries_host) *lt_entries_host = host[0];
+  if (pair_count_host) *pair_count_host = host[1];
+  if (host[0] > f->lt_capacity || host[1] > f->pair_capacity)
+    return fail(GART_ERR_CAPACITY, "need lt %lld (have %lld), pairs %lld (have %lld)", (long long)host[0],
+                (long long)f->lt_capacity, (long long)host[1], (long long)f->pair_capacity);
+  if (host[1] >= (int64_t(1) << 32)) return fail(GART_ERR_UNSUPPORTED, "more than 2^32 tile pairs");
+  f->stage = 1;
+  return GART_OK;
+}
+
+gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* settings, gart_frame* f,
+                                void* stream) {
+  g_err[0] = 0;
+  gart_status st;
+  if ((st = check_camera(camera)) != GART_OK) return st;
+  if ((st = check_settings(settings)) != GART_OK) return st;
+  GART_REQUIRE(f != nullptr, "frame is NULL");
+  GART_REQUIRE(f->stage >= 1, "gart_bounds must succeed on this frame first");
+  GART_REQUIRE(f->tiles_x == tiles_along(camera->width, settings->tile) &&
+                   f->tiles_y == tiles_along(camera->height, settings->tile),
+               "camera/tile differ from gart_bounds");
+  const int64_t n = f->n, P = f->pair_count;
+  const int64_t n_tiles = int64_t(f->tiles_x) * f->tiles_y;
+  GART_REQUIRE(f->pair_offset && f->tile_range, "frame pair_offset/tile_range is NULL");
+  GART_REQUIRE(P <= f->pair_capacity, "pair capacity");
+  if (P > 0) GART_REQUIRE(f->pair_tile && f->pair_prim, "frame pair buffers are NULL");
+  const int K = (f->sh_degree + 1) * (f->sh_degree + 1);
+  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode);
+  GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  uint32_t* key = at<uint32_t>(f->scratch, L.depth_key);
+  uint32_t* perm = at<uint32_t>(f->scratch, L.perm);
+  GART_HIP(iota_u32(perm, n, s));
+  GART_HIP(radix_sort_u32(key, perm, at<uint32_t>(f->scratch, L.key_alt), at<uint32_t>(f->scratch, L.perm_alt), n,
+                          32, at<void>(f->scratch, L.radix_tmp), s));
+  TileMapArgs T{};
+  T.n = n;
+  T.tile = settings->tile;
+  T.tiles_x = f->tiles_x;
+  T.tiles_y = f->tiles_y;
+  T.rect = f->rect;
+  T.tile_count = f->tile_count;
+  T.perm = perm;
+  T.base_rank = at<int64_t>(f->scratch, L.base_rank);
+  T.pair_offset = f->pair_offset;
+  T.keys = f->pair_tile;
+  T.vals = f->pair_prim;
+  T.pair_count = P;
+  T.tile_range = f->tile_range;
+  GART_HIP(launch_gather_counts(T, s));
+  GART_HIP(scan_exclusive_i64(T.base_rank, T.base_rank, n, T.base_rank + n, at<void>(f->scratch, L.scan_tmp), s));
+  GART_HIP(launch_scatter_pair_offset(T, s));
+  GART_HIP(launch_emit_pairs(T, s));
+  int bits = 1;
+  while ((int64_t(1) << bits) < n_tiles) ++bits;
+  GART_HIP(radix_sort_u32(f->pair_tile, f->pair_prim, at<uint32_t>(f->scratch, L.pair_key_alt),
+                          at<uint32_t>(f->scratch, L.pair_val_alt), P, bits, at<void>(f->scratch, L.radix_tmp), s));
+  GART_HIP(launch_tile_ranges(f->pair_tile, P, n_tiles, f->tile_range, s));
+  f->stage = 2;
+  return GART_OK;
+}
+
+gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                         gart_frame* f, float* image, void* stream) {
+  g_err[0] = 0;
+  gart_status st;
+  if ((st = check_gaussians(g)) != GART_OK) return st;
+  if ((st = check_camera(camera)) != GART_OK) return st;
+  if ((st = check_settings(settings)) != GART_OK) return st;
+  GART_REQUIRE(f != nullptr, "frame is NULL");
+  GART_REQUIRE(f->stage >= 2, "gart_build_tile_map must succeed on this frame first");
+  GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
+  GART_REQUIRE(image != nullptr && f->pixel_state != nullptr, "image/pixel_state is NULL");
+  GART_REQUIRE(f->lt_entries <= f->lt_capacity, "lt capacity");
+  GART_REQUIRE(f->lt_entries == 0 || (f->lt != nullptr && aligned16(f->lt)), "lt must be non-NULL, 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ForwardArgs A{};
+  A.cam = make_cam(camera);
+  A.tile = settings->tile;
+  A.tiles_x = f->tiles_x;
+  A.tiles_y = f->tiles_y;
+  A.sh_k = (g->sh_degree + 1) * (g->sh_degree + 1);
+  A.t_min = settings->t_min;
+  A.tile_range = f->tile_range;
+  A.pair_prim = f->pair_prim;
+  A.geom = f->prim_geom;
+  A.rect = f->rect;
+  A.lt_offset = f->lt_offset;
+  A.sh = g->sh;
+  A.lt = reinterpret_cast<float4*>(f->lt);
+  A.image = image;
+  A.pixel_state = f->pixel_state;
+  A.counters = f->counters;
+  GART_HIP(launch_forward(A, s));
+  f->stage = 3;
+  return GART_OK;
+}
+
+gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                          const gart_frame* f, const float* image, const float* dL_dimage, float* g_means,
+                          float* g_log_scales, float* g_quats, float* g_logits, float* g_sh, void* stream) {
+  g_err[0] = 0;
+  gart_status st;
+  if ((st = check_gaussians(g)) != GART_OK) return st;
+  if ((st = check_camera(camera)) != GART_OK) return st;
+  if ((st = check_settings(settings)) != GART_OK) return st;
+  GART_REQUIRE(f != nullptr, "frame is NULL");
+  GART_REQUIRE(f->stage >= 3, "gart_forward must succeed on this frame first");
+  GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
+  GART_REQUIRE(image && dL_dimage, "image/dL_dimage is NULL");
+  if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
+  const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
+  const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode);
+  GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu (backward mode %d)", f->scratch_bytes,
+               L.total, settings->backward_mode);
+  GART_REQUIRE(aligned16(f->scratch), "scratch must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  BackwardArgs A{};
+  A.cam = make_cam(camera);
+  A.tile = settings->tile;
+  A.tiles_x = f->tiles_x;
+  A.tiles_y = f->tiles_y;
+  A.sh_k = K;
+  A.mode = settings->backward_mode;
+  A.n = f->n;
+  A.tile_range = f->tile_range;
+  A.pair_prim = f->pair_prim;
+  A.geom = f->prim_geom;
+  A.rect = f->rect;
+  A.lt_offset = f->lt_offset;
+  A.pair_offset = f->pair_offset;
+  A.tile_count = f->tile_count;
+  A.sh = g->sh;
+  A.lt = reinterpret_cast<const float4*>(f->lt);
+  A.image = image;
+  A.dl_dimage = dL_dimage;
+  A.pixel_state = f->pixel_state;
+  A.acc = at<float>(f->scratch, L.acc);
+  A.rows = at<float>(f->scratch, L.rows);
+  A.row_flag = at<uint8_t>(f->scratch, L.row_flag);
+  A.pair_count = f->pair_count;
+  A.log_scales = g->log_scales;
+  A.quats = g->quats;
+  A.g_means = g_means;
+  A.g_log_scales = g_log_scales;
+  A.g_quats = g_quats;
+  A.g_logits = g_logits;
+  A.g_sh = g_sh;
+  A.counters = f->counters;
+  GART_HIP(launch_backward(A, s));
+  return GART_OK;
+}
+
+}  // extern "C"

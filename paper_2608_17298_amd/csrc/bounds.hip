@@ -1,0 +1,278 @@
+// Per-Gaussian pre-processing and the tile-primitive map.
+//
+// bounds_kernel: one thread per Gaussian, fp64.  Rotation from the
+// normalised quaternion, scales, opacity, clamp radius alpha_c (Sec. 3.4,
+// Eq. 9-10), the world-to-Gaussian map W = S^-1 R^T and o_g = W (o - mu)
+// (Eq. 5, "w2g" pre-computation of Sec. 5.3), and the conservative pixel
+// rectangle from the projected dual quadric (Sec. 4.2, Eq. 11-14).
+//
+// Tile map (Sec. 4.3, reverse tile mapping): pairs are emitted in order of
+// a per-Gaussian depth lower bound so that, after the stable sort by tile
+// id, every tile's list is ordered front to back.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "ops.h"
+
+namespace gart {
+namespace {
+
+constexpr double kRectPad = 1e-4;  // pixels added on each side of a rectangle
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Pixel index range [lo, hi] covered on one image axis.  The plane through
+// the camera containing the pixel line u (clip-space X - u w = 0) meets the
+// ellipsoid iff q(u) = Qaa - 2 u Qa4 + u^2 Q44 >= 0.  With Q44 < 0 (the eye
+// plane misses the ellipsoid) that is u in [p - h, p + h], p = Qa4 / Q44,
+// h = sqrt(p^2 - Qaa / Q44) (Eq. 12-14).  With Q44 >= 0 the ellipsoid crosses
+// the eye plane: the covered set is u <= u1 or u >= u2 (or all u), and the
+// range is the hull of the covered pixel centres.
+__device__ bool axis_cover(double Qaa, double Qa4, double Q44, int npix, int* lo, int* hi) {
+  const double e = kRectPad;
+  const double last = double(npix - 1);
+  double a, b;
+  if (Q44 < 0.0) {
+    const double p = Qa4 / Q44;
+    const double h = sqrt(fmax(0.0, p * p - Qaa / Q44));
+    a = fmax(ceil(p - h - 0.5 - e), 0.0);
+    b = fmin(floor(p + h - 0.5 + e), last);
+  } else if (Q44 == 0.0) {
+    if (Qa4 == 0.0) {
+      if (!(Qaa >= 0.0)) return false;
+      a = 0.0;
+      b = last;
+    } else {
+      const double r = Qaa / (2.0 * Qa4);
+      if (Qa4 > 0.0) {
+        a = 0.0;
+        b = fmin(floor(r - 0.5 + e), last);
+      } else {
+        a = fmax(ceil(r - 0.5 - e), 0.0);
+        b = last;
+      }
+    }
+  } else {
+    const double disc = Qa4 * Qa4 - Q44 * Qaa;
+    if (disc <= 0.0) {
+      a = 0.0;
+      b = last;
+    } else {
+      const double sq = sqrt(disc);
+      const double u1 = (Qa4 - sq) / Q44, u2 = (Qa4 + sq) / Q44;
+      const bool left = (u1 - 0.5 + e) >= 0.0;
+      const bool right = (u2 - 0.5 - e) <= last;
+      if (!left && !right) return false;
+      a = left ? 0.0 : fmax(ceil(u2 - 0.5 - e), 0.0);
+      b = right ? last : fmin(floor(u1 - 0.5 + e), last);
+    }
+  }
+  if (a > b) return false;
+  *lo = int(a);
+  *hi = int(b);
+  return true;
+}
+
+__global__ __launch_bounds__(256) void bounds_kernel(BoundsArgs A) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  uint32_t my_tiles = 0;
+  if (i < A.n) {
+    const CamParams& c = A.cam;
+    float mf[3], lf[3], qf[4];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      mf[k] = A.means[3 * i + k];
+      lf[k] = A.log_scales[3 * i + k];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) qf[k] = A.quats[4 * i + k];
+    const float lg = A.logits[i];
+    bool ok = isfinite(lg);
+#pragma unroll
+    for (int k = 0; k < 3; ++k) ok = ok && isfinite(mf[k]) && isfinite(lf[k]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) ok = ok && isfinite(qf[k]);
+    const double qw = qf[0], qx = qf[1], qy = qf[2], qz = qf[3];
+    const double qq = qw * qw + qx * qx + qy * qy + qz * qz;
+    ok = ok && qq > 0.0;
+    const double sigma = 1.0 / (1.0 + exp(-double(lg)));
+    ok = ok && sigma > A.alpha_min;
+
+    double* G = A.geom + kGeomStride * i;
+    int rx0 = 0, ry0 = 0, rx1 = -1, ry1 = -1;
+    float key = __int_as_float(0x7f800000);  // +inf: culled Gaussians sort last
+    if (ok) {
+      const double inv = 1.0 / sqrt(qq);
+      const double w = qw * inv, x = qx * inv, y = qy * inv, z = qz * inv;
+      // R(q), row-major
+      const double R[9] = {1.0 - 2.0 * (y * y + z * z), 2.0 * (x * y - w * z), 2.0 * (x * z + w * y),
+                           2.0 * (x * y + w * z), 1.0 - 2.0 * (x * x + z * z), 2.0 * (y * z - w * x),
+                           2.0 * (x * z - w * y), 2.0 * (y * z + w * x), 1.0 - 2.0 * (x * x + y * y)};
+      const double s[3] = {exp(double(lf[0])), exp(double(lf[1])), exp(double(lf[2]))};
+      const double mu[3] = {mf[0], mf[1], mf[2]};
+      const double D2c = 2.0 * log(sigma / A.alpha_min);
+      const double ac = sqrt(D2c);
+
+      // Projected transform rows T'_a = V_a [R S alpha_c | mu] for the X, Y
+      // and w rows of the pixel-clip matrix, and the dual-quadric entries
+      // <v, T'_a . T'_b>, v = (1, 1, 1, -1).
+      double Tp[3][4];
+      const double* V[3] = {c.V0, c.V1, c.V3};
+#pragma unroll
+      for (int a = 0; a < 3; ++a) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+          Tp[a][k] = (V[a][0] * R[k] + V[a][1] * R[3 + k] + V[a][2] * R[6 + k]) * (s[k] * ac);
+        Tp[a][3] = V[a][0] * mu[0] + V[a][1] * mu[1] + V[a][2] * mu[2] + V[a][3];
+      }
+      auto Q = [&](int a, int b) {
+        return Tp[a][0] * Tp[b][0] + Tp[a][1] * Tp[b][1] + Tp[a][2] * Tp[b][2] - Tp[a][3] * Tp[b][3];
+      };
+      const double Q44 = Q(2, 2);
+      const bool behind = Q44 < 0.0 && Tp[2][3] <= 0.0;
+      bool vis = !behind;
+      if (vis) vis = axis_cover(Q(0, 0), Q(0, 2), Q44, c.W, &rx0, &rx1);
+      if (vis) vis = axis_cover(Q(1, 1), Q(1, 2), Q44, c.H, &ry0, &ry1);
+      if (vis) {
+        // W = S^-1 R^T, o_g = W (o - mu)
+        const double om[3] = {c.o[0] - mu[0], c.o[1] - mu[1], c.o[2] - mu[2]};
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          const double is = 1.0 / s[k];
+          const double w0 = R[k] * is, w1 = R[3 + k] * is, w2 = R[6 + k] * is;
+          G[kGeoW + 3 * k + 0] = w0;
+          G[kGeoW + 3 * k + 1] = w1;
+          G[kGeoW + 3 * k + 2] = w2;
+          G[kGeoOg + k] = w0 * om[0] + w1 * om[1] + w2 * om[2];
+        }
+        G[kGeoD2c] = D2c;
+        G[kGeoSigma] = sigma;
+        // Any hit point lies inside the ball of radius alpha_c max(s) around
+        // mu, so its depth along the unit ray is at least |mu - o| - r.
+        const double dist = sqrt(om[0] * om[0] + om[1] * om[1] + om[2] * om[2]);
+        const double r = ac * fmax(s[0], fmax(s[1], s[2]));
+        const double lo = dist - r - 1e-12 * (dist + r);
+        key = lo > 0.0 ? __double2float_rd(lo) : 0.0f;
+        G[kGeoKey] = double(key);
+        const int ts = A.tile;
+        my_tiles = uint32_t(rx1 / ts - rx0 / ts + 1) * uint32_t(ry1 / ts - ry0 / ts + 1);
+      } else {
+        rx0 = ry0 = 0;
+        rx1 = ry1 = -1;
+      }
+    }
+    if (my_tiles == 0) {
+#pragma unroll
+      for (int k = 0; k < kGeomStride; ++k) G[k] = 0.0;
+      G[kGeoD2c] = -1.0;  // no ray can pass the hit test
+      G[kGeoKey] = double(__int_as_float(0x7f800000));
+      key = __int_as_float(0x7f800000);
+      rx0 = ry0 = 0;
+      rx1 = ry1 = -1;
+    }
+    A.rect[4 * i + 0] = rx0;
+    A.rect[4 * i + 1] = ry0;
+    A.rect[4 * i + 2] = rx1;
+    A.rect[4 * i + 3] = ry1;
+    A.area[i] = my_tiles ? int64_t(rx1 - rx0 + 1) * int64_t(ry1 - ry0 + 1) : 0;
+    A.tile_count[i] = my_tiles;
+    A.depth_key[i] = __float_as_uint(key);
+  }
+  // block sum of tile counts -> one atomic per wave
+  unsigned long long t = my_tiles;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) t += __shfl_xor(t, off);
+  if (__lane_id() == 0 && t) atomicAdd(A.pair_total, t);
+}
+
+__global__ void gather_counts_kernel(TileMapArgs A) {
+  const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r < A.n) A.base_rank[r] = A.tile_count[A.perm[r]];
+}
+
+__global__ void scatter_pair_offset_kernel(TileMapArgs A) {
+  const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r < A.n) A.pair_offset[A.perm[r]] = A.base_rank[r];
+  if (r == 0) A.pair_offset[A.n] = A.base_rank[A.n];
+}
+
+// One block emits the pairs of 256 consecutive depth ranks; its threads
+// stride over the block's pair slots and find their rank by binary search
+// over the ranks' first slots held in LDS.
+constexpr int kEmitRanks = 256;
+
+__global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
+  __shared__ int64_t s_base[kEmitRanks + 1];
+  __shared__ int32_t s_rect[kEmitRanks][4];
+  __shared__ uint32_t s_prim[kEmitRanks];
+  const int64_t r0 = int64_t(blockIdx.x) * kEmitRanks;
+  const int nr = int(std::min<int64_t>(kEmitRanks, A.n - r0));
+  for (int k = threadIdx.x; k <= nr; k += blockDim.x) s_base[k] = A.base_rank[r0 + k];
+  for (int k = threadIdx.x; k < nr; k += blockDim.x) {
+    const uint32_t p = A.perm[r0 + k];
+    s_prim[k] = p;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) s_rect[k][c] = A.rect[4 * int64_t(p) + c];
+  }
+  __syncthreads();
+  const int64_t first = s_base[0], last = s_base[nr];
+  const int ts = A.tile;
+  for (int64_t j = first + threadIdx.x; j < last; j += blockDim.x) {
+    int lo = 0, hi = nr - 1;  // largest k with s_base[k] <= j
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_base[mid] <= j) lo = mid; else hi = mid - 1;
+    }
+    const int k = lo;
+    const int64_t q = j - s_base[k];
+    const int tx0 = s_rect[k][0] / ts, ty0 = s_rect[k][1] / ts, tx1 = s_rect[k][2] / ts;
+    const int ntx = tx1 - tx0 + 1;
+    const int tx = tx0 + int(q % ntx), ty = ty0 + int(q / ntx);
+    A.keys[j] = uint32_t(ty) * uint32_t(A.tiles_x) + uint32_t(tx);
+    A.vals[j] = s_prim[k];
+  }
+}
+
+// tile_range[t] = first sorted pair whose tile id is >= t.
+__global__ void tile_ranges_kernel(const uint32_t* __restrict__ keys, int64_t m, int64_t n_tiles,
+                                   int64_t* __restrict__ range) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j > m) return;
+  const int64_t prev = (j == 0) ? -1 : int64_t(keys[j - 1]);
+  const int64_t cur = (j == m) ? n_tiles : int64_t(keys[j]);
+  for (int64_t t = prev + 1; t <= cur && t <= n_tiles; ++t) range[t] = j;
+}
+
+}  // namespace
+
+hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  bounds_kernel<<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_counts(const TileMapArgs& a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  gather_counts_kernel<<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_pair_offset(const TileMapArgs& a, hipStream_t s) {
+  scatter_pair_offset_kernel<<<std::max<int64_t>(1, ceil_div(a.n, 256)), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.pair_count <= 0) return hipSuccess;
+  emit_pairs_kernel<<<ceil_div(a.n, kEmitRanks), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tile_ranges(const uint32_t* sorted_keys, int64_t pair_count, int64_t n_tiles, int64_t* tile_range,
+                              hipStream_t s) {
+  tile_ranges_kernel<<<ceil_div(pair_count + 1, 256), 256, 0, s>>>(sorted_keys, pair_count, n_tiles, tile_range);
+  return hipGetLastError();
+}
+
+}  // namespace gart

@@ -1,0 +1,141 @@
+// Device-side building blocks shared by the GART kernels (gfx950, wave64).
+//
+// Every routine that decides a discrete outcome (ray direction, hit test,
+// depth) is written once here and used unchanged by the forward trace and
+// by both backward variants, so the backward re-derives exactly the hits the
+// forward composited.  The library is compiled with -ffp-contract=off;
+// fused multiply-adds appear only where written explicitly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/gart.h"
+
+namespace gart {
+
+constexpr int kGeomStride = 16;  // doubles per Gaussian in prim_geom
+// prim_geom layout (double): [0..8] W = S^-1 R^T row-major, [9..11] o_g =
+// W (o - mu), [12] squared clamp radius D2c, [13] opacity sigma, [14] depth
+// lower bound (the float sort key, widened), [15] unused.
+constexpr int kGeoW = 0, kGeoOg = 9, kGeoD2c = 12, kGeoSigma = 13, kGeoKey = 14;
+
+constexpr uint32_t kNoPrim = 0xffffffffu;
+
+// Camera constants, computed on the host in double from the float inputs.
+struct CamParams {
+  double o[3];        // camera centre in world space, o = -R^T t
+  double Rt[9];       // R^T row-major (camera -> world rotation)
+  double fx, fy, cx, cy;
+  double V0[4], V1[4], V3[4];  // rows of the world -> pixel-clip matrix (X, Y, w)
+  int32_t W, H;
+};
+
+// Gradient values accumulated per Gaussian before the chain rule:
+// [0..2] sum 2u x_g, [3..8] sum 2u x_g x_g^T (xx, yy, zz, xy, xz, yz),
+// [9] dL/dsigma, [10..10+3K) dL/dsh.  Rows are padded to a multiple of 4.
+__host__ __device__ constexpr int acc_width(int K) { return 10 + 3 * K; }
+__host__ __device__ constexpr int acc_stride(int K) { return (acc_width(K) + 3) & ~3; }
+
+// Unit world-space ray direction through the centre of pixel (px, py).
+__device__ __forceinline__ void pixel_ray(const CamParams& c, int px, int py, double d[3]) {
+  const double a = (double(px) + 0.5 - c.cx) / c.fx;
+  const double b = (double(py) + 0.5 - c.cy) / c.fy;
+  double v[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) v[k] = fma(c.Rt[3 * k], a, fma(c.Rt[3 * k + 1], b, c.Rt[3 * k + 2]));
+  const double inv = 1.0 / sqrt(fma(v[0], v[0], fma(v[1], v[1], v[2] * v[2])));
+#pragma unroll
+  for (int k = 0; k < 3; ++k) d[k] = v[k] * inv;
+}
+
+// Max-response point of a Gaussian on the ray o + tau d (Eq. 4-5) in the
+// Gaussian's normalised frame: d_g = W d, tau = -<o_g, d_g> / <d_g, d_g>,
+// x_g = o_g + tau d_g, D2 = |x_g|^2.  Returns the hit decision tau > 0 and
+// D2 <= D2c (alpha >= alpha_min).
+__device__ __forceinline__ bool ray_hit(const double W[9], const double og[3], double D2c, const double d[3],
+                                        double* tau_out, double* D2_out, double xg[3]) {
+  double dg[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) dg[k] = fma(W[3 * k], d[0], fma(W[3 * k + 1], d[1], W[3 * k + 2] * d[2]));
+  const double num = fma(og[0], dg[0], fma(og[1], dg[1], og[2] * dg[2]));
+  const double den = fma(dg[0], dg[0], fma(dg[1], dg[1], dg[2] * dg[2]));
+  const double tau = -num / den;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) xg[k] = fma(tau, dg[k], og[k]);
+  const double D2 = fma(xg[0], xg[0], fma(xg[1], xg[1], xg[2] * xg[2]));
+  *tau_out = tau;
+  *D2_out = D2;
+  return tau > 0.0 && D2 <= D2c;
+}
+
+// (tau, id) lexicographic order used to composite hits.
+__device__ __forceinline__ bool key_less(double t1, uint32_t i1, double t2, uint32_t i2) {
+  return t1 < t2 || (t1 == t2 && i1 < i2);
+}
+
+// Real spherical harmonics without Condon-Shortley phase, index l*l + l + m,
+// as polynomials of the unit direction (x, y, z).
+template <int K>
+__device__ __forceinline__ void sh_basis(float x, float y, float z, float Y[K]) {
+  Y[0] = 0.28209479177387814f;
+  if constexpr (K > 1) {
+    Y[1] = 0.4886025119029199f * y;
+    Y[2] = 0.4886025119029199f * z;
+    Y[3] = 0.4886025119029199f * x;
+  }
+  if constexpr (K > 4) {
+    const float xx = x * x, yy = y * y, zz = z * z;
+    Y[4] = 1.0925484305920792f * x * y;
+    Y[5] = 1.0925484305920792f * y * z;
+    Y[6] = 0.31539156525252005f * (3.0f * zz - 1.0f);
+    Y[7] = 1.0925484305920792f * x * z;
+    Y[8] = 0.5462742152960396f * (xx - yy);
+    if constexpr (K > 9) {
+      Y[9] = 0.5900435899266435f * y * (3.0f * xx - yy);
+      Y[10] = 2.890611442640554f * x * y * z;
+      Y[11] = 0.4570457994644658f * y * (5.0f * zz - 1.0f);
+      Y[12] = 0.3731763325901154f * z * (5.0f * zz - 3.0f);
+      Y[13] = 0.4570457994644658f * x * (5.0f * zz - 1.0f);
+      Y[14] = 1.445305721320277f * z * (xx - yy);
+      Y[15] = 0.5900435899266435f * x * (xx - 3.0f * yy);
+    }
+  }
+}
+
+// Offset of pixel (px, py) inside the block of Gaussian i's intermediate
+// buffer entries, relative to O_prim(i) (Eq. 16): O_tile + O_pixel with the
+// rectangle's tiles in row-major order and pixels row-major inside a tile.
+__device__ __forceinline__ int64_t lt_local_index(int x0, int y0, int x1, int y1, int ts, int px, int py) {
+  const int tx = px / ts, ty = py / ts;
+  const int ya = max(y0, ty * ts), yb = min(y1, ty * ts + ts - 1);
+  const int xa = max(x0, tx * ts), xb = min(x1, tx * ts + ts - 1);
+  const int64_t o_tile = int64_t(x1 - x0 + 1) * (ya - y0) + int64_t(yb - ya + 1) * (xa - x0);
+  const int64_t o_pix = int64_t(py - ya) * (xb - xa + 1) + (px - xa);
+  return o_tile + o_pix;
+}
+
+// Block index -> tile index such that each of the 8 XCDs (which receive
+// blocks round-robin) works on one contiguous band of tiles and keeps the
+// band's Gaussians in its own L2.
+__device__ __forceinline__ int xcd_tile(int b, int n) {
+  const int q = n / 8, r = n % 8;
+  const int x = b % 8, k = b / 8;
+  // XCD x owns tiles [x*q + min(x, r), ...) of length q + (x < r)
+  return x * q + min(x, r) + k;
+}
+
+__device__ __forceinline__ unsigned lane_id() { return __lane_id(); }
+
+// Adds a per-lane count to a device counter with one atomic per wave.  Must
+// be called with the whole wave active.
+__device__ __forceinline__ void count_add(uint64_t* ctr, uint32_t v) {
+  if (ctr == nullptr) return;
+  unsigned long long s = v;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane_id() == 0 && s) atomicAdd(reinterpret_cast<unsigned long long*>(ctr), static_cast<unsigned long long>(s));
+}
+
+}  // namespace gart

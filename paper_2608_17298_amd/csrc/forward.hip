@@ -1,0 +1,292 @@
+// Forward software trace (Sec. 3.2-3.3, Eq. 3-8) writing the (L, T)
+// intermediate buffer in primitive-major order (Sec. 4.3, Eq. 16).
+//
+// One workgroup per tile, one lane per pixel.  The tile's Gaussian list is
+// ordered by a conservative lower bound on the depth at which each Gaussian
+// can be hit, so a lane can stream it front to back with a small sorted hit
+// buffer held in registers: a buffered hit is final -- and is composited --
+// as soon as its depth is below the lower bound of the next Gaussian in the
+// list.  The result is exactly the (tau, index) order.  If the buffer
+// overflows, the largest hits are dropped and the lane later rescans the
+// list from the first Gaussian it dropped, skipping hits already
+// composited; compositing stops once the transmittance falls below t_min.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+
+#include "ops.h"
+
+namespace gart {
+namespace {
+
+constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
+// Each rescan composites at least one hit per rescanning lane, so the pass
+// count is bounded by the hits of a tile; this cap only guards against a
+// defect turning into a hang.
+constexpr int kMaxPasses = 1 << 20;
+// row: [0..8] W, [9..11] o_g, [12] D2c, [13] sigma, [14] depth key,
+// [15] O_prim (int64 bits), [16..17] rect (4 x int32), [18] index (uint32)
+
+template <int TILE, int K>
+__global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
+  constexpr int NT = TILE * TILE;
+  constexpr int KB = 8;  // per-lane hit buffer (registers)
+  constexpr double kInf = __builtin_huge_val();
+
+  __shared__ __align__(16) double s_row[NT * kRow];
+  __shared__ float s_key[NT + 1];
+  __shared__ unsigned s_restart;
+
+  const int n_tiles = A.tiles_x * A.tiles_y;
+  const int tile = xcd_tile(blockIdx.x, n_tiles);
+  const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
+  const int tid = threadIdx.x;
+  const int px = tx * TILE + tid % TILE, py = ty * TILE + tid / TILE;
+  const bool valid = px < A.cam.W && py < A.cam.H;
+
+  double d[3];
+  pixel_ray(A.cam, valid ? px : 0, valid ? py : 0, d);
+  float Y[K];
+  sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
+
+  const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
+
+  double T = 1.0, L0 = 0.0, L1 = 0.0, L2 = 0.0;
+  bool done = !valid;     // terminated (or no pixel)
+  bool finished = false;  // every hit composited
+  bool stalled = false;   // must wait for a rescan
+  uint32_t n_hits = 0, n_tests = 0;
+  double last_tau = -kInf;
+  uint32_t last_id = 0;
+  double end_tau = kInf;
+  uint32_t end_id = kNoPrim;
+
+  double bt[KB], ba[KB];
+  int64_t bi[KB];
+  uint32_t bid[KB], bc[KB];
+  int cnt = 0;
+  double e_tau = kInf;  // smallest dropped hit (all buffered hits are smaller)
+  uint32_t e_id = kNoPrim;
+  uint32_t jr = UINT_MAX;  // first list position holding a dropped hit
+#pragma unroll
+  for (int s = 0; s < KB; ++s) {
+    bt[s] = kInf;
+    ba[s] = 0.0;
+    bi[s] = 0;
+    bid[s] = kNoPrim;
+    bc[s] = 0;
+  }
+
+  auto drop = [&](double t, uint32_t id, uint32_t c) {
+    if (key_less(t, id, e_tau, e_id)) {
+      e_tau = t;
+      e_id = id;
+    }
+    jr = min(jr, c);
+  };
+
+  auto composite_front = [&]() {
+    const double a = ba[0];
+    const uint32_t id = bid[0];
+    const float* shp = A.sh + int64_t(id) * (3 * K);
+    float c[3];
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+      float v = 0.5f;
+#pragma unroll
+      for (int k = 0; k < K; ++k) v = fmaf(shp[3 * k + ch], Y[k], v);
+      c[ch] = fmaxf(v, 0.0f);
+    }
+    A.lt[bi[0]] = make_float4(float(L0), float(L1), float(L2), float(T));
+    const double w = T * a;
+    L0 = fma(w, double(c[0]), L0);
+    L1 = fma(w, double(c[1]), L1);
+    L2 = fma(w, double(c[2]), L2);
+    T = T * (1.0 - a);
+    ++n_hits;
+    last_tau = bt[0];
+    last_id = id;
+    if (T < A.t_min) {
+      done = true;
+      end_tau = bt[0];
+      end_id = id;
+    }
+#pragma unroll
+    for (int s = 0; s + 1 < KB; ++s) {
+      bt[s] = bt[s + 1];
+      ba[s] = ba[s + 1];
+      bi[s] = bi[s + 1];
+      bid[s] = bid[s + 1];
+      bc[s] = bc[s + 1];
+    }
+    --cnt;
+  };
+
+  uint32_t restart = 0;
+  int passes = 0;
+  for (;;) {
+    for (int64_t base = beg + restart; base < end; base += NT) {
+      const int nb = int(min<int64_t>(NT, end - base));
+      if (tid < nb) {
+        const uint32_t id = A.pair_prim[base + tid];
+        const double* G = A.geom + int64_t(kGeomStride) * id;
+        double* row = s_row + tid * kRow;
+#pragma unroll
+        for (int k = 0; k < 15; ++k) row[k] = G[k];
+        row[15] = __longlong_as_double(A.lt_offset[id]);
+        const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
+        int* ri = reinterpret_cast<int*>(row + 16);
+        ri[0] = r.x;
+        ri[1] = r.y;
+        ri[2] = r.z;
+        ri[3] = r.w;
+        reinterpret_cast<uint32_t*>(row + 18)[0] = id;
+        s_key[tid] = float(G[kGeoKey]);
+      }
+      if (tid == 0) {
+        const int64_t nx = base + nb;
+        s_key[nb] = (nx < end) ? float(A.geom[int64_t(kGeomStride) * A.pair_prim[nx] + kGeoKey])
+                               : __int_as_float(0x7f800000);
+      }
+      __syncthreads();
+      if (!done && !finished && !stalled) {
+        for (int c = 0; c < nb; ++c) {
+          const double* row = s_row + c * kRow;
+          const int4 r = *reinterpret_cast<const int4*>(row + 16);
+          if (px >= r.x && px <= r.z && py >= r.y && py <= r.w) {
+            ++n_tests;
+            double W[9], og[3];
+#pragma unroll
+            for (int k = 0; k < 9; ++k) W[k] = row[k];
+#pragma unroll
+            for (int k = 0; k < 3; ++k) og[k] = row[9 + k];
+            double tau, D2, xg[3];
+            const uint32_t id = reinterpret_cast<const uint32_t*>(row + 18)[0];
+            if (ray_hit(W, og, row[12], d, &tau, &D2, xg) && key_less(last_tau, last_id, tau, id)) {
+              const uint32_t cpos = uint32_t(base - beg) + uint32_t(c);
+              if (!key_less(tau, id, e_tau, e_id)) {
+                drop(tau, id, cpos);
+              } else {
+                bool ins = true;
+                if (cnt == KB) {
+                  if (!key_less(tau, id, bt[KB - 1], bid[KB - 1])) {
+                    drop(tau, id, cpos);
+                    ins = false;
+                  } else {
+                    drop(bt[KB - 1], bid[KB - 1], bc[KB - 1]);
+                    cnt = KB - 1;
+                  }
+                }
+                if (ins) {
+                  const double a = row[13] * exp(-0.5 * D2);
+                  const int64_t li = __double_as_longlong(row[15]) +
+                                     lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py);
+                  int pos = 0;
+#pragma unroll
+                  for (int s = 0; s < KB; ++s) pos += (s < cnt && key_less(bt[s], bid[s], tau, id)) ? 1 : 0;
+#pragma unroll
+                  for (int s = KB - 1; s >= 1; --s) {
+                    if (s > pos && s <= cnt) {
+                      bt[s] = bt[s - 1];
+                      ba[s] = ba[s - 1];
+                      bi[s] = bi[s - 1];
+                      bid[s] = bid[s - 1];
+                      bc[s] = bc[s - 1];
+                    }
+                  }
+#pragma unroll
+                  for (int s = 0; s < KB; ++s) {
+                    if (s == pos) {
+                      bt[s] = tau;
+                      ba[s] = a;
+                      bi[s] = li;
+                      bid[s] = id;
+                      bc[s] = cpos;
+                    }
+                  }
+                  ++cnt;
+                }
+              }
+            }
+          }
+          const double nk = double(s_key[c + 1]);
+          while (cnt > 0 && bt[0] < nk && !done) composite_front();
+          if (done) break;
+          if (e_tau < kInf && nk > e_tau) {
+            stalled = true;
+            break;
+          }
+        }
+      }
+      const bool busy = !done && !finished && !stalled;
+      if (!__syncthreads_or(busy)) break;
+    }
+    // End of pass: every buffered hit is below the smallest dropped one and
+    // no unscanned Gaussian can precede it.
+    while (cnt > 0 && !done) composite_front();
+    const bool need = !done && !finished && e_tau < kInf;
+    if (!done && !need) finished = true;
+    if (tid == 0) s_restart = UINT_MAX;
+    __syncthreads();
+    if (need) atomicMin(&s_restart, jr);
+    __syncthreads();
+    const unsigned rs = s_restart;
+    __syncthreads();
+    if (rs == UINT_MAX || passes >= kMaxPasses) break;
+    restart = rs;
+    ++passes;
+    if (need) {
+      e_tau = kInf;
+      e_id = kNoPrim;
+      jr = UINT_MAX;
+      stalled = false;
+      cnt = 0;
+    }
+  }
+
+  if (valid) {
+    const int64_t p = int64_t(py) * A.cam.W + px;
+    A.image[3 * p + 0] = float(L0);
+    A.image[3 * p + 1] = float(L1);
+    A.image[3 * p + 2] = float(L2);
+    gart_pixel_state st;
+    st.tau_end = end_tau;
+    st.id_end = end_id;
+    st.n_hits = n_hits;
+    A.pixel_state[p] = st;
+  }
+  if (A.counters) {
+    count_add(A.counters + GART_CNT_FWD_HITS, n_hits);
+    count_add(A.counters + GART_CNT_FWD_TESTS, n_tests);
+    if (tid == 0 && passes)
+      atomicAdd(reinterpret_cast<unsigned long long*>(A.counters + GART_CNT_FWD_RESCANS), (unsigned long long)passes);
+  }
+}
+
+template <int TILE, int K>
+hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
+  const int n_tiles = a.tiles_x * a.tiles_y;
+  forward_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+template <int TILE>
+hipError_t launch_k(const ForwardArgs& a, hipStream_t s) {
+  switch (a.sh_k) {
+    case 1: return launch_t<TILE, 1>(a, s);
+    case 4: return launch_t<TILE, 4>(a, s);
+    case 9: return launch_t<TILE, 9>(a, s);
+    case 16: return launch_t<TILE, 16>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_forward(const ForwardArgs& a, hipStream_t s) {
+  if (a.tiles_x * a.tiles_y <= 0) return hipSuccess;
+  return a.tile == 16 ? launch_k<16>(a, s) : launch_k<8>(a, s);
+}
+
+}  // namespace gart

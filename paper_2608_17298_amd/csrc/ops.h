@@ -1,0 +1,125 @@
+// Host-side launchers shared between the library's translation units.
+// Every launcher enqueues on `s` and returns the first HIP error it sees.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "common.h"
+
+namespace gart {
+
+// ---- scan.hip / sort ------------------------------------------------------
+// Exclusive prefix sum of n values (in may equal out).  If total is not
+// null, the sum of all n values is stored at *total (device).  tmp must hold
+// scan_tmp_bytes(n) bytes.
+size_t scan_tmp_bytes(int64_t n);
+hipError_t scan_exclusive_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp, hipStream_t s);
+hipError_t scan_exclusive_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total, void* tmp, hipStream_t s);
+
+// Stable LSD radix sort of (key, value) pairs on key bits [0, bits), 8 bits
+// per pass.  The sorted pairs end in (keys, vals); (keys_alt, vals_alt) are
+// scratch of the same length.  tmp must hold radix_tmp_bytes(m) bytes.
+size_t radix_tmp_bytes(int64_t m);
+hipError_t radix_sort_u32(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt, int64_t m, int bits,
+                          void* tmp, hipStream_t s);
+
+// Simple fills and gathers.
+hipError_t fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+hipError_t fill_f32(float* p, float v, int64_t n, hipStream_t s);
+hipError_t fill_u8(uint8_t* p, uint8_t v, int64_t n, hipStream_t s);
+hipError_t iota_u32(uint32_t* p, int64_t n, hipStream_t s);
+
+// ---- bounds.hip ----------------------------------------------------------
+struct BoundsArgs {
+  const float* means;
+  const float* log_scales;
+  const float* quats;
+  const float* logits;
+  int64_t n;
+  CamParams cam;
+  double alpha_min;
+  int32_t tile;
+  int32_t* rect;
+  int64_t* area;            // [n] rectangle areas (scanned later into O_prim)
+  double* geom;
+  uint32_t* tile_count;
+  uint32_t* depth_key;      // [n] float bits of the depth lower bound
+  unsigned long long* pair_total;  // device accumulator of sum tile_count
+};
+hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s);
+
+struct TileMapArgs {
+  int64_t n;
+  int32_t tile, tiles_x, tiles_y;
+  const int32_t* rect;
+  const uint32_t* tile_count;
+  const uint32_t* perm;     // [n] Gaussian index at each depth rank
+  int64_t* base_rank;       // [n+1] scratch: first pair slot per rank (scanned in place)
+  int64_t* pair_offset;     // [n+1] output: first pair slot per Gaussian index
+  uint32_t* keys;           // [P] emitted tile ids
+  uint32_t* vals;           // [P] emitted Gaussian indices
+  int64_t pair_count;
+  int64_t* tile_range;      // [n_tiles+1]
+};
+hipError_t launch_gather_counts(const TileMapArgs& a, hipStream_t s);
+hipError_t launch_scatter_pair_offset(const TileMapArgs& a, hipStream_t s);
+hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s);
+hipError_t launch_tile_ranges(const uint32_t* sorted_keys, int64_t pair_count, int64_t n_tiles, int64_t* tile_range,
+                              hipStream_t s);
+
+// ---- forward.hip -------------------------------------------------------
+struct ForwardArgs {
+  CamParams cam;
+  int32_t tile, tiles_x, tiles_y, sh_k;
+  double t_min;
+  const int64_t* tile_range;
+  const uint32_t* pair_prim;
+  const double* geom;
+  const int32_t* rect;
+  const int64_t* lt_offset;
+  const float* sh;
+  float4* lt;
+  float* image;
+  gart_pixel_state* pixel_state;
+  uint64_t* counters;
+};
+hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);
+
+// ---- backward.hip ------------------------------------------------------
+struct BackwardArgs {
+  CamParams cam;
+  int32_t tile, tiles_x, tiles_y, sh_k, mode;
+  int64_t n;
+  const int64_t* tile_range;
+  const uint32_t* pair_prim;
+  const double* geom;
+  const int32_t* rect;
+  const int64_t* lt_offset;
+  const int64_t* pair_offset;
+  const uint32_t* tile_count;
+  const float* sh;
+  const float4* lt;
+  const float* image;
+  const float* dl_dimage;
+  const gart_pixel_state* pixel_state;
+  // gradient accumulation
+  float* acc;          // [n, acc_stride] per-Gaussian accumulators (atomic modes)
+  float* rows;         // [P, acc_stride] per-pair partial rows (gather mode)
+  uint8_t* row_flag;   // [P] 1 if the pair's row was written
+  int64_t pair_count;
+  // raw inputs and outputs
+  const float* log_scales;
+  const float* quats;
+  float* g_means;
+  float* g_log_scales;
+  float* g_quats;
+  float* g_logits;
+  float* g_sh;
+  uint64_t* counters;
+};
+hipError_t launch_backward(const BackwardArgs& a, hipStream_t s);
+
+}  // namespace gart

@@ -48,3 +48,54 @@ def random_tiny_scene(rng, n, w, h, deg, tile=8, spread=0.6, ls_mu=-2.3, ls_sd=0
     sc = custom_scene(means, ls, q, logits, sh, cam, tile=tile, dl_dimage=dl)
     params = dict(means=means, log_scales=ls, quats=q, opacity_logits=logits, sh=sh)
     return sc, params, dl
+
+
+def l1_upstream(scene, oracle_mod):
+    """dL/dC of an L1 loss against a render of the perturbed-means copy,
+    sign(C - C*), both rendered by the oracle (sign(0) = 0)."""
+    import oracle as _o  # noqa: F401  (tests only)
+    o = oracle_mod.OracleScene(scene)
+    C = o.render()["color"]
+    pert = oracle_mod.OracleScene(scene, params=dict(means=scene.means_perturbed.astype(np.float64)))
+    Cs = pert.render()["color"]
+    return np.sign(C - Cs).reshape(scene.camera.height, scene.camera.width, 3).astype(np.float32)
+
+
+def run_gpu(scene, mode="gather", tile=None, dl=None, counters=True, keep_frame=False):
+    """Run the four C-ABI calls on cuda:0 and return host copies of the outputs."""
+    import torch
+    from paper_2608_17298_amd import gart
+    cam = gart.make_camera(scene.camera)
+    st = gart.make_settings(tile or scene.tile, mode)
+    g = gart.Gaussians.from_scene(scene)
+    frame = gart.prepare(g, cam, st, counters=counters)
+    image = torch.empty((cam.height, cam.width, 3), dtype=torch.float32, device="cuda")
+    gart.gart_forward(g, cam, st, frame, image)
+    dlt = torch.from_numpy(np.ascontiguousarray(scene.dl_dimage if dl is None else dl, dtype=np.float32)).cuda()
+    grads = gart.empty_grads(g)
+    gart.gart_backward(g, cam, st, frame, image, dlt, grads)
+    torch.cuda.synchronize()
+    n = scene.n
+    P = frame.pair_count
+    ps = frame.pixel_state.cpu().numpy()
+    out = dict(
+        rect=frame.rect.cpu().numpy()[:n], lt_offset=frame.lt_offset.cpu().numpy()[:n + 1],
+        tile_count=frame.tile_count.cpu().numpy()[:n].view(np.uint32), geom=frame.prim_geom.cpu().numpy()[:n],
+        pair_tile=frame.pair_tile.cpu().numpy()[:P].view(np.uint32),
+        pair_prim=frame.pair_prim.cpu().numpy()[:P].view(np.uint32),
+        pair_offset=frame.pair_offset.cpu().numpy()[:n + 1], tile_range=frame.tile_range.cpu().numpy(),
+        image=image.cpu().numpy(), tau_end=ps[:, 0].copy().view(np.float64),
+        id_end=(ps[:, 1] & 0xffffffff).astype(np.int64),
+        n_hits=(ps[:, 1] >> 32).astype(np.int64), lt_entries=frame.lt_entries, pair_count=P,
+        grads={k: v.cpu().numpy().astype(np.float64) for k, v in grads.items()},
+        counters=None if frame.counters is None else frame.counters.cpu().numpy())
+    if keep_frame:
+        out["frame"] = frame
+    return out
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)

@@ -1,0 +1,242 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Bars: rectangles, areas, offsets and per-tile Gaussian sets bit-exact;
+pixels within 1e-5 max-abs outside ambiguous pixels (decision margin below
+1e-9, counted); each gradient group within 1e-4 relative L2.
+Sizes span several tiles with a ragged edge; the oracle finishes in seconds.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import dc_for_colour, l1_upstream, random_tiny_scene, rel_l2, run_gpu, small_camera
+from paper_2608_17298_amd.scenes import custom_scene, make_scene
+
+pytestmark = pytest.mark.gpu
+
+PIX_TOL = 1e-5
+GRAD_TOL = 1e-4
+AMBIG = 1e-9
+GROUPS = ["means", "log_scales", "quats", "logits", "sh"]
+
+
+def _scene(name):
+    if name == "tiny":
+        return make_scene("tiny")
+    if name == "small_reduced":
+        sc = make_scene("small", n=30000, width=203, height=157)
+        sc.dl_dimage = l1_upstream(sc, oracle)
+        return sc
+    if name == "1m_reduced":
+        sc = make_scene("1m", n=120000, width=171, height=115)
+        sc.dl_dimage = l1_upstream(sc, oracle)
+        return sc
+    if name == "stress_reduced":
+        sc = make_scene("stress", n=6000, width=97, height=75)
+        sc.dl_dimage = l1_upstream(sc, oracle)
+        return sc
+    if name == "random_sh3":
+        sc, _, _ = random_tiny_scene(np.random.default_rng(5), 300, 83, 61, 3, spread=1.0, ls_mu=-2.6,
+                                     ls_sd=0.5, logit_mu=1.0)
+        return sc
+    raise KeyError(name)
+
+
+_cache = {}
+
+
+def _case(name, mode="gather", tile=None):
+    key = (name, mode, tile)
+    if key not in _cache:
+        sc = _cache.get(("scene", name)) or _scene(name)
+        _cache[("scene", name)] = sc
+        if ("oracle", name) not in _cache:
+            o = oracle.OracleScene(sc)
+            _cache[("oracle", name)] = (o, o.prim_info(), o.render(), o.backward(sc.dl_dimage))
+        _cache[key] = run_gpu(sc, mode=mode, tile=tile)
+    o, info, ren, grads = _cache[("oracle", name)]
+    return _cache[("scene", name)], o, info, ren, grads, _cache[key]
+
+
+SCENES = ["tiny", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3"]
+
+
+@pytest.mark.parametrize("name", SCENES)
+def test_bounds_bit_exact(name):
+    sc, o, info, ren, grads, gpu = _case(name)
+    assert np.array_equal(gpu["rect"], info.rect)
+    area = np.diff(gpu["lt_offset"])
+    assert np.array_equal(area, info.area)
+    assert gpu["lt_offset"][0] == 0 and gpu["lt_entries"] == info.area.sum()
+
+
+@pytest.mark.parametrize("name", SCENES)
+def test_tile_lists_bit_exact(name):
+    sc, o, info, ren, grads, gpu = _case(name)
+    ts = sc.tile
+    off, prim = oracle.tile_lists(info.rect, info.state, o.W, o.H, ts)
+    assert np.array_equal(gpu["tile_range"], off)
+    assert gpu["pair_count"] == len(prim)
+    key = gpu["geom"][:, 14]
+    gp = gpu["pair_prim"].astype(np.int64)
+    for t in range(len(off) - 1):
+        seg = gp[off[t]:off[t + 1]]
+        assert np.array_equal(np.sort(seg), prim[off[t]:off[t + 1]]), t
+        k = key[seg]
+        # front-to-back order inside a tile: depth lower bound, then index
+        assert np.all((np.diff(k) > 0) | ((np.diff(k) == 0) & (np.diff(seg) > 0))), t
+    assert np.all(gpu["pair_tile"][:-1] <= gpu["pair_tile"][1:])
+    # pair_offset: each Gaussian owns tile_count consecutive emission slots
+    act = np.nonzero(info.area > 0)[0]
+    po = gpu["pair_offset"]
+    order = act[np.argsort(po[act], kind="stable")]
+    assert np.array_equal(np.diff(np.append(po[order], po[-1])), gpu["tile_count"][order].astype(np.int64))
+
+
+@pytest.mark.parametrize("name", SCENES)
+def test_forward_pixels_and_markers(name):
+    sc, o, info, ren, grads, gpu = _case(name)
+    img = gpu["image"].reshape(-1, 3)
+    ok = ren["margin"] >= AMBIG
+    err = np.abs(img - ren["color"]).max(axis=1)
+    assert err[ok].max() <= PIX_TOL, (err[ok].max(), np.argmax(np.where(ok, err, 0)))
+    assert (~ok).sum() <= max(2, 1e-3 * ok.size)
+    assert np.array_equal(gpu["n_hits"][ok], ren["n_included"][ok])
+    term = np.isfinite(ren["tau_end"]) & ok
+    assert np.array_equal(gpu["id_end"][term], ren["id_end"][term])
+    assert np.all(~np.isfinite(gpu["tau_end"][~np.isfinite(ren["tau_end"]) & ok]))
+
+
+@pytest.mark.parametrize("name", ["tiny", "small_reduced", "random_sh3"])
+def test_forward_lt_entries(name):
+    """(L, T) written at idx(i,t,p) for every composited hit (Eq. 16)."""
+    import torch
+    sc, o, info, ren, grads, _ = _case(name)
+    gpu = run_gpu(sc, keep_frame=True)
+    ok = np.nonzero(ren["margin"] >= AMBIG)[0]
+    pix = ok[ren["n_included"][ok] > 0][:20000]
+    off, prim, LT, tau = o.records(pix, ren["n_included"][pix])
+    owner = np.repeat(pix, np.diff(off))
+    idx = o.lt_index(sc.tile, prim, owner)
+    assert (idx >= 0).all()
+    lt = gpu["frame"].lt[torch.from_numpy(idx).cuda()].cpu().numpy().astype(np.float64)
+    assert np.abs(lt[:, :3] - LT[:, :3]).max() <= PIX_TOL
+    assert np.abs(lt[:, 3] - LT[:, 3]).max() <= 1e-6
+
+
+@pytest.mark.parametrize("mode", ["gather", "gather_atomic", "scatter"])
+@pytest.mark.parametrize("name", SCENES)
+def test_backward_parity(name, mode):
+    sc, o, info, ren, grads, gpu = _case(name, mode)
+    for k in GROUPS:
+        e = rel_l2(gpu["grads"][k], grads[k])
+        assert e <= GRAD_TOL, (k, e)
+
+
+def test_gather_deterministic():
+    sc = _scene("random_sh3")
+    a = run_gpu(sc, mode="gather")
+    b = run_gpu(sc, mode="gather")
+    for k in GROUPS:
+        assert np.array_equal(a["grads"][k], b["grads"][k]), k
+
+
+@pytest.mark.parametrize("tile", [8, 16])
+def test_tile_sizes_agree(tile):
+    sc, o, info, ren, grads, _ = _case("small_reduced")
+    gpu = run_gpu(sc, tile=tile)
+    ok = ren["margin"] >= AMBIG
+    assert np.abs(gpu["image"].reshape(-1, 3) - ren["color"])[ok].max() <= PIX_TOL
+    for k in GROUPS:
+        assert rel_l2(gpu["grads"][k], grads[k]) <= GRAD_TOL, k
+
+
+def test_counters_match_oracle():
+    sc, o, info, ren, grads, gpu = _case("small_reduced")
+    c = gpu["counters"]
+    assert abs(int(c[0]) - int(ren["n_included"].sum())) <= 10
+    assert c[3] == c[0]  # the backward visits exactly the composited hits
+
+
+# ---------------------------------------------------------------------------
+# Edge cases
+# ---------------------------------------------------------------------------
+def _mini(means, ls, logit, w=19, h=13, deg=0, tile=8):
+    n = len(means)
+    q = np.tile([1.0, 0.2, -0.1, 0.3], (n, 1))
+    sh = np.zeros((n, (deg + 1) ** 2, 3))
+    sh[:, 0, :] = dc_for_colour(0.6)
+    dl = np.random.default_rng(0).standard_normal((h, w, 3))
+    return custom_scene(means, ls, q, logit, sh, small_camera(w, h), tile=tile, dl_dimage=dl)
+
+
+def test_empty_scene():
+    sc = _mini(np.zeros((0, 3)), np.zeros((0, 3)), np.zeros(0))
+    gpu = run_gpu(sc)
+    assert gpu["pair_count"] == 0 and gpu["lt_entries"] == 0
+    assert np.all(gpu["image"] == 0)
+    assert all(v.size == 0 for v in gpu["grads"].values())
+
+
+def test_all_culled():
+    means = np.array([[0, 0, 0], [0.1, 0, 0], [0, 0, -9.0]])
+    ls = np.full((3, 3), -2.0)
+    logit = np.array([-8.0, -9.0, 2.0])  # two below alpha_min, one behind the camera
+    sc = _mini(means, ls, logit)
+    gpu = run_gpu(sc)
+    assert gpu["pair_count"] == 0
+    assert np.all(gpu["image"] == 0)
+    assert all(np.all(v == 0) for v in gpu["grads"].values())
+
+
+def test_one_pixel_image_and_camera_inside():
+    means = np.array([[0, 0, -4.0], [0.0, 0.0, 0.0], [0.02, -0.01, 1.0]])
+    ls = np.log(np.array([[0.6, 0.5, 0.7], [0.3, 0.3, 0.3], [0.2, 0.25, 0.3]]))
+    logit = np.array([-1.0, 0.5, 1.5])
+    for (w, h) in [(1, 1), (9, 17)]:
+        sc = _mini(means, ls, logit, w=w, h=h, deg=1)
+        o = oracle.OracleScene(sc)
+        ren = o.render()
+        gpu = run_gpu(sc)
+        assert np.abs(gpu["image"].reshape(-1, 3) - ren["color"]).max() <= PIX_TOL
+        g = o.backward(sc.dl_dimage)
+        for k in GROUPS:
+            assert rel_l2(gpu["grads"][k], g[k]) <= GRAD_TOL, (w, h, k)
+
+
+def test_capacity_error_then_growth():
+    import torch
+    from paper_2608_17298_amd import gart
+    sc = _scene("tiny")
+    cam = gart.make_camera(sc.camera)
+    st = gart.make_settings(sc.tile)
+    g = gart.Gaussians.from_scene(sc)
+    f = gart.Frame(g.n, g.sh_degree, cam, st, lt_capacity=10, pair_capacity=10)
+    with pytest.raises(gart.GartCapacityError) as ei:
+        gart.gart_bounds(g, cam, st, f)
+    e = ei.value
+    assert e.lt_entries == oracle.OracleScene(sc).lt_total() and e.pair_count > 10
+    with pytest.raises(gart.GartError):  # a failed gart_bounds leaves the frame unusable
+        gart.gart_build_tile_map(cam, st, f)
+    f.grow(e.lt_entries, e.pair_count, 1.0)
+    assert gart.gart_bounds(g, cam, st, f) == (e.lt_entries, e.pair_count)
+    gart.gart_build_tile_map(cam, st, f)
+    img = torch.empty((cam.height, cam.width, 3), device="cuda")
+    gart.gart_forward(g, cam, st, f, img)
+
+
+def test_invalid_args_on_device_path():
+    import torch
+    from paper_2608_17298_amd import gart
+    sc = _scene("tiny")
+    cam = gart.make_camera(sc.camera)
+    g = gart.Gaussians.from_scene(sc)
+    st = gart.make_settings(16)
+    f = gart.prepare(g, cam, st)
+    img = torch.empty((cam.height, cam.width, 3), device="cuda")
+    with pytest.raises(gart.GartError):  # backward before forward
+        gart.gart_backward(g, cam, st, f, img, img, gart.empty_grads(g))
+    bad = gart.make_settings(16)
+    bad.t_min = 0.0
+    with pytest.raises(gart.GartError):
+        gart.gart_forward(g, cam, bad, f, img)

@@ -1,0 +1,94 @@
+"""CPU checks of the built C-ABI library: it loads without a GPU, exports
+every function declared in include/gart.h, and rejects invalid arguments
+before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "gart.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(gart_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2608_17298_amd import gart
+    return gart.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"gart_bounds", "gart_build_tile_map", "gart_forward", "gart_backward"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    from paper_2608_17298_amd import gart
+    for code, name in [(0, "GART_OK"), (-1, "GART_ERR_INVALID_ARG"), (-2, "GART_ERR_CAPACITY"),
+                       (-3, "GART_ERR_HIP"), (-4, "GART_ERR_UNSUPPORTED")]:
+        assert gart.lib().gart_status_string(code).decode() == name
+
+
+def _structs(tile=8, mode=0, n=0, deg=0, w=16, h=16):
+    from paper_2608_17298_amd import gart
+    from helpers import small_camera
+    cam = gart.make_camera(small_camera(w, h))
+    st = gart.make_settings(tile, mode)
+    g = gart.gart_gaussians()
+    g.n, g.sh_degree = n, deg
+    f = gart.gart_frame()
+    return cam, st, g, f
+
+
+@pytest.mark.parametrize("bad", ["tile", "mode", "alpha", "tmin", "width", "fx", "deg", "nptr", "frame"])
+def test_invalid_arguments_rejected_on_host(lib, bad):
+    cam, st, g, f = _structs()
+    fp = ctypes.byref(f)
+    if bad == "tile":
+        st.tile = 12
+    elif bad == "mode":
+        st.backward_mode = 5
+    elif bad == "alpha":
+        st.alpha_min = 0.0
+    elif bad == "tmin":
+        st.t_min = 1.5
+    elif bad == "width":
+        cam.width = 0
+    elif bad == "fx":
+        cam.fx = -1.0
+    elif bad == "deg":
+        g.sh_degree = 4
+    elif bad == "nptr":
+        g.n = 10  # non-zero count with null parameter pointers
+    elif bad == "frame":
+        fp = None
+    r = lib.gart_bounds(ctypes.byref(g), ctypes.byref(cam), ctypes.byref(st), fp, None, None, None)
+    expect = -4 if bad == "deg" else -1
+    assert r == expect, (bad, r, lib.gart_last_error())
+    assert lib.gart_last_error().decode() != ""
+
+
+def test_call_order_enforced(lib):
+    cam, st, g, f = _structs()
+    assert lib.gart_build_tile_map(ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f), None) == -1
+    img = ctypes.c_float(0)
+    assert lib.gart_forward(ctypes.byref(g), ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f),
+                            ctypes.byref(img), None) == -1
+
+
+def test_scratch_bytes_monotone(lib):
+    from paper_2608_17298_amd import gart
+    cam, st, g, f = _structs()
+    a = gart.gart_scratch_bytes(1000, 3, 10_000, cam, st)
+    b = gart.gart_scratch_bytes(1000, 3, 100_000, cam, st)
+    c = gart.gart_scratch_bytes(100_000, 3, 100_000, cam, st)
+    assert 0 < a < b < c
+    st.backward_mode = 1
+    assert gart.gart_scratch_bytes(1000, 3, 100_000, cam, st) < b  # no per-pair rows needed
