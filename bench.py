@@ -1,0 +1,333 @@
+#!/usr/bin/env python3
+"""Benchmark of the 3DGART hot path on one MI355X.
+
+A step is one pass of the whole path over the 1M-Gaussian synthetic scene
+(1,000,000 Gaussians, SH degree 3, 1237x822, 8x8 tiles): gart_bounds ->
+gart_build_tile_map -> gart_forward -> gart_backward, inputs resident in
+HBM.  The headline value is backward Gaussian-pixel gradients per second
+(composited hits / backward time); ms_per_step is the whole fwd+bwd
+iteration.  Kernel times come from HIP events that the library records on
+its own stream around each kernel.
+
+Prints one JSON line.  ``--gpus N`` with N > 1 exits: this path runs on one
+GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_PEAK_TFLOPS = 157.3       # MI355X vector FP32
+FP64_PEAK_TFLOPS = 78.6        # MI355X vector FP64
+
+# Algorithmic cost model (per unit of work).
+F64_PER_TEST = 40              # ray/Gaussian max-response test in fp64 (W d, two dots, tau, x_g, D2, compare)
+GEOM_BYTES = 128 + 16 + 8 + 4  # per visited pair: fp64 geometry row, rect, O_prim, pair index
+
+
+def f32_per_hit_bwd(K):
+    # colour 6K, per-hit gradient terms ~25, AW products (9 + 3K), AW accumulations (10 + 3K)
+    return 6 * K + 25 + (9 + 3 * K) + (10 + 3 * K)
+
+
+def f32_per_hit_fwd(K):
+    return 6 * K + 10  # colour, compositing (the exp and T update counted as fp64)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="1m", choices=["tiny", "small", "1m", "4m", "stress"])
+    ap.add_argument("--mode", default="gather", choices=["gather", "gather_atomic", "scatter"])
+    ap.add_argument("--compare-modes", type=int, default=1, help="also time the other backward modes")
+    ap.add_argument("--cpu-baseline", type=int, default=1)
+    ap.add_argument("--cpu-pixels", type=int, default=0, help="oracle sample size in pixels (0 = whole frame)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a device copy of this size (HBM counter calibration) and exit")
+    ap.add_argument("--out", default=None, help="also write the JSON line to this file")
+    return ap.parse_args()
+
+
+def copy_probe(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, device="cuda", dtype=torch.float32)
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_per_dispatch": n * 4}))
+
+
+def source_hash(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {
+    "gather": ["paper_2608_17298_amd/csrc/backward.hip", "paper_2608_17298_amd/csrc/common.h"],
+    "forward": ["paper_2608_17298_amd/csrc/forward.hip", "paper_2608_17298_amd/csrc/common.h"],
+}
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if absent or if the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(f"{kernel}/{workload}")
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha256") != source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding is a design only).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_17298_amd import gart
+    from paper_2608_17298_amd.scenes import make_scene
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
+
+    t0 = time.time()
+    sc = make_scene(args.workload)
+    K = sc.sh_k
+    cam = gart.make_camera(sc.camera)
+    st = gart.make_settings(sc.tile, args.mode)
+    g = gart.Gaussians.from_scene(sc)
+    stream = torch.cuda.current_stream()
+    H, W = sc.camera.height, sc.camera.width
+    print(f"[bench] scene {args.workload}: N={sc.n} K={K} {W}x{H} tile {sc.tile}, generated in "
+          f"{time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    # Upstream gradient: L1 loss against a render of the perturbed-means copy
+    # (rendered once with the same pipeline, outside the timed region).
+    gp = gart.Gaussians.from_scene(sc)
+    gp.means = torch.from_numpy(sc.means_perturbed).cuda()
+    fp = gart.prepare(gp, cam, st)
+    target = torch.empty((H, W, 3), dtype=torch.float32, device="cuda")
+    gart.gart_forward(gp, cam, st, fp, target)
+    del fp
+
+    frame = gart.prepare(g, cam, st, slack=1.05)
+    image = torch.empty((H, W, 3), dtype=torch.float32, device="cuda")
+    gart.gart_forward(g, cam, st, frame, image)
+    dl = torch.sign(image - target).contiguous()
+    grads = gart.empty_grads(g)
+
+    # Counting run (device counters; not timed).
+    frame.counters = torch.zeros(gart.NUM_COUNTERS, dtype=torch.int64, device="cuda")
+    counts = {}
+    for mode in (["gather", "gather_atomic", "scatter"] if args.compare_modes else [args.mode]):
+        frame.counters.zero_()
+        stm = gart.make_settings(sc.tile, mode)
+        gart.gart_bounds(g, cam, stm, frame)
+        gart.gart_build_tile_map(cam, stm, frame)
+        gart.gart_forward(g, cam, stm, frame, image)
+        gart.gart_backward(g, cam, stm, frame, image, dl, grads)
+        torch.cuda.synchronize()
+        counts[mode] = frame.counters.cpu().numpy().astype(np.int64)
+    frame.counters = None
+    c = counts[args.mode]
+    hits = int(c[gart.CNT_FWD_HITS])
+
+    def make_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record(stream)  # materialise the underlying hipEvent_t
+        return evs
+
+    def run_steps(settings, n_steps, n_warm, backward_only=False):
+        per = []
+        for s in range(n_warm + n_steps):
+            timed = s >= n_warm
+            if timed:
+                call = make_events(5)
+                kern = make_events(gart.NUM_EVENTS)
+                frame.set_events([e.cuda_event for e in kern])
+            else:
+                frame.set_events([])
+            if not backward_only:
+                if timed:
+                    call[0].record(stream)
+                gart.gart_bounds(g, cam, settings, frame)
+                if timed:
+                    call[1].record(stream)
+                gart.gart_build_tile_map(cam, settings, frame)
+                if timed:
+                    call[2].record(stream)
+                gart.gart_forward(g, cam, settings, frame, image)
+            if timed:
+                call[3].record(stream)
+            gart.gart_backward(g, cam, settings, frame, image, dl, grads)
+            if timed:
+                call[4].record(stream)
+                per.append((call, kern))
+        frame.set_events([])
+        torch.cuda.synchronize()
+        return per
+
+    def ms(a, b):
+        return a.elapsed_time(b)
+
+    # Warm-up, then exactly K timed steps bracketed by synchronisation.
+    run_steps(st, 0, args.warmup)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    per = run_steps(st, args.steps, 0)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_per_step = 1e3 * wall / args.steps
+
+    def avg(fn):
+        return float(np.mean([fn(cl, kr) for cl, kr in per]))
+
+    call_ms = dict(
+        bounds=avg(lambda cl, kr: ms(cl[0], cl[1])), tile_map=avg(lambda cl, kr: ms(cl[1], cl[2])),
+        forward=avg(lambda cl, kr: ms(cl[2], cl[3])), backward=avg(lambda cl, kr: ms(cl[3], cl[4])))
+    kern_ms = dict(
+        pair_sort=avg(lambda cl, kr: ms(kr[0], kr[1])), forward_trace=avg(lambda cl, kr: ms(kr[2], kr[3])),
+        backward_main=avg(lambda cl, kr: ms(kr[4], kr[5])), reduce_chain=avg(lambda cl, kr: ms(kr[6], kr[7])))
+
+    # Algorithmic work of the two dominant kernels.
+    npix = W * H
+    AW = 10 + 3 * K
+    AS = (AW + 3) & ~3
+    bwd_tests, bwd_hits = int(c[gart.CNT_BWD_TESTS]), int(c[gart.CNT_BWD_HITS])
+    bwd_pairs, bwd_active = int(c[gart.CNT_BWD_PAIRS]), int(c[gart.CNT_BWD_ACTIVE])
+    fwd_tests = int(c[gart.CNT_FWD_TESTS])
+    work = {
+        "backward_main": dict(
+            bytes=16 * bwd_hits + bwd_pairs * (GEOM_BYTES + 12 * K) + bwd_active * (4 * AS + 1) + npix * (12 + 12 + 16),
+            f64=F64_PER_TEST * bwd_tests, f32=f32_per_hit_bwd(K) * bwd_hits),
+        "forward_trace": dict(
+            bytes=16 * hits + int(frame.pair_count) * GEOM_BYTES + npix * (12 + 16) + hits * 12 * K,
+            f64=F64_PER_TEST * fwd_tests + 30 * hits, f32=f32_per_hit_fwd(K) * hits),
+    }
+
+    def roofline(name):
+        w = work[name]
+        t = kern_ms[name] * 1e-3
+        t_hbm = w["bytes"] / (HBM_PEAK_GBS * 1e9)
+        t_alu = w["f32"] / (FP32_PEAK_TFLOPS * 1e12) + w["f64"] / (FP64_PEAK_TFLOPS * 1e12)
+        if t_hbm >= t_alu:
+            achieved = w["bytes"] / t / 1e9
+            return dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                        frac=round(achieved / HBM_PEAK_GBS, 4))
+        flops = w["f32"] + w["f64"]
+        peak = flops / t_alu / 1e12  # mix-weighted ALU peak for this kernel's fp32/fp64 split
+        achieved = flops / t / 1e12
+        return dict(bound="alu", achieved=round(achieved, 3), peak=round(peak, 1), unit="TFLOP/s",
+                    frac=round(achieved / peak, 4), f32_flops=w["f32"], f64_flops=w["f64"],
+                    hbm_bytes_algorithmic=w["bytes"])
+
+    dominant = max(("forward_trace", "backward_main"), key=lambda k: kern_ms[k])
+    roof = roofline(dominant)
+    roof["kernel"] = "gather_kernel" if dominant == "backward_main" else "forward_kernel"
+    roof["traffic"] = recorded_traffic("gather" if dominant == "backward_main" else "forward", args.workload)
+
+    value = bwd_hits / (call_ms["backward"] * 1e-3)
+
+    modes = {}
+    if args.compare_modes:
+        for mode in ("gather", "gather_atomic", "scatter"):
+            stm = gart.make_settings(sc.tile, mode)
+            per_m = run_steps(stm, max(5, args.steps // 2), 2, backward_only=True)
+            bms = float(np.mean([ms(cl[3], cl[4]) for cl, kr in per_m]))
+            kms = float(np.mean([ms(kr[4], kr[5]) for cl, kr in per_m]))
+            cm = counts[mode]
+            modes[mode] = dict(backward_ms=round(bms, 4), main_kernel_ms=round(kms, 4),
+                               grads_per_s=round(int(cm[gart.CNT_BWD_HITS]) / (bms * 1e-3), 1),
+                               float_atomics=int(cm[gart.CNT_BWD_ATOMICS]))
+
+    cpu = None
+    if args.cpu_baseline:
+        cpu = cpu_baseline(sc, dl.cpu().numpy(), args.cpu_pixels)
+
+    line = {
+        "metric": "backward Gaussian-pixel grads/sec; ms per fwd+bwd iter @1M Gaussians",
+        "value": round(value, 1),
+        "unit": "grads/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+f64",
+        "data": "synthetic (seeded generator; stands in for Mip-NeRF 360)",
+        "config": {"workload": f"{args.workload}: {sc.n} Gaussians, SH{sc.sh_degree}, {W}x{H}, "
+                               f"{sc.tile}x{sc.tile} tiles", "backward_mode": args.mode,
+                   "composited_hits": hits, "pairs": int(frame.pair_count), "lt_entries": int(frame.lt_entries)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "call_ms": {k: round(v, 4) for k, v in call_ms.items()},
+        "kernel_ms": {k: round(v, 4) for k, v in kern_ms.items()},
+        "grads_per_s_full_step": round(hits / (ms_per_step * 1e-3), 1),
+        "backward_modes": modes,
+        "forward_rescans": int(c[gart.CNT_FWD_RESCANS]),
+        "counters": {name: int(c[i]) for i, name in enumerate(
+            ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
+             "bwd_active_pairs"])},
+        "kernels_roofline": {k: roofline(k) for k in work},
+    }
+    s = json.dumps(line)
+    print(s, flush=True)
+    if args.out:
+        with open(args.out, "w") as f:
+            f.write(s + "\n")
+
+
+def cpu_baseline(sc, dl, npix):
+    """The fp64 oracle (untuned) on a bounded pixel sample of the same workload:
+    its per-pixel forward + analytic backward over every candidate."""
+    import oracle
+    rng = np.random.default_rng(7)
+    W, H = sc.camera.width, sc.camera.height
+    if npix <= 0 or npix >= W * H:
+        pix = np.arange(W * H)
+    else:
+        pix = np.sort(rng.choice(W * H, size=npix, replace=False))
+    o = oracle.OracleScene(sc)
+    hits = int(o.render(pix)["n_included"].sum())
+    t = time.perf_counter()
+    o.backward(dl, pixels=pix)
+    dt = time.perf_counter() - t
+    return {"value": round(hits / dt, 1), "unit": "grads/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{len(pix)} pixels of the same frame ({hits} composited hits), "
+                      f"fp64 forward+backward per pixel, {dt:.1f}s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -125,6 +125,10 @@ typedef struct {
   size_t scratch_bytes;
   /* optional device counters (NULL = not counted), uint64[GART_NUM_COUNTERS] */
   uint64_t* counters;
+  /* optional hipEvent_t handles (NULL = not recorded), see GART_EV_*: the
+   * library records each on `stream` immediately before / after the named
+   * kernel, so a caller can time single kernels on the library's stream */
+  void* events[8];
   /* [out] host-side totals and call-order state, filled by the library */
   int64_t n;              /* Gaussians seen by gart_bounds */
   int32_t sh_degree;
@@ -142,7 +146,20 @@ enum {
   GART_CNT_BWD_TESTS = 4,     /* (pixel, Gaussian) ray tests in the backward */
   GART_CNT_BWD_ATOMICS = 5,   /* float atomic adds issued by the backward */
   GART_CNT_BWD_PAIRS = 6,     /* (tile, prim) pairs visited by the backward */
+  GART_CNT_BWD_ACTIVE = 7,    /* visited pairs with at least one composited hit */
   GART_NUM_COUNTERS = 8
+};
+
+enum {
+  GART_EV_SORT_BEGIN = 0,   /* radix sort of the (tile, prim) pairs (all passes) */
+  GART_EV_SORT_END = 1,
+  GART_EV_FWD_BEGIN = 2,    /* forward trace kernel */
+  GART_EV_FWD_END = 3,
+  GART_EV_BWD_BEGIN = 4,    /* backward main kernel (gather or scatter) */
+  GART_EV_BWD_END = 5,
+  GART_EV_REDUCE_BEGIN = 6, /* per-Gaussian reduction and chain rule */
+  GART_EV_REDUCE_END = 7,
+  GART_NUM_EVENTS = 8
 };
 
 /* Bytes of scratch a frame needs for n Gaussians of the given SH degree and

@@ -266,8 +266,10 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   GART_HIP(launch_emit_pairs(T, s));
   int bits = 1;
   while ((int64_t(1) << bits) < n_tiles) ++bits;
+  GART_HIP(record(f->events[GART_EV_SORT_BEGIN], s));
   GART_HIP(radix_sort_u32(f->pair_tile, f->pair_prim, at<uint32_t>(f->scratch, L.pair_key_alt),
                           at<uint32_t>(f->scratch, L.pair_val_alt), P, bits, at<void>(f->scratch, L.radix_tmp), s));
+  GART_HIP(record(f->events[GART_EV_SORT_END], s));
   GART_HIP(launch_tile_ranges(f->pair_tile, P, n_tiles, f->tile_range, s));
   f->stage = 2;
   return GART_OK;
@@ -304,6 +306,8 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.image = image;
   A.pixel_state = f->pixel_state;
   A.counters = f->counters;
+  A.ev_begin = f->events[GART_EV_FWD_BEGIN];
+  A.ev_end = f->events[GART_EV_FWD_END];
   GART_HIP(launch_forward(A, s));
   f->stage = 3;
   return GART_OK;
@@ -360,6 +364,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.g_logits = g_logits;
   A.g_sh = g_sh;
   A.counters = f->counters;
+  for (int k = 0; k < 4; ++k) A.ev[k] = f->events[GART_EV_BWD_BEGIN + k];
   GART_HIP(launch_backward(A, s));
   return GART_OK;
 }

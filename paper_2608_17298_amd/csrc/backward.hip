@@ -141,7 +141,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   for (int w = 1; w < NT / 64; ++w) tmax = fmax(tmax, s_wmax[w]);
 
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
-  uint32_t n_pairs = 0, n_hits = 0, n_tests = 0, n_atom = 0;
+  uint32_t n_pairs = 0, n_hits = 0, n_tests = 0, n_atom = 0, n_active = 0;
   for (int64_t j = beg + tid; j < end; j += NT) {
     const uint32_t i = A.pair_prim[j];
     const double* G = A.geom + int64_t(kGeomStride) * i;
@@ -188,6 +188,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       }
     }
     if (!any) continue;
+    ++n_active;
     if constexpr (ATOMIC) {
       float* dst = A.acc + int64_t(i) * AS;
 #pragma unroll
@@ -211,6 +212,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   }
   if (A.counters) {
     count_add(A.counters + GART_CNT_BWD_PAIRS, n_pairs);
+    count_add(A.counters + GART_CNT_BWD_ACTIVE, n_active);
     count_add(A.counters + GART_CNT_BWD_HITS, n_hits);
     count_add(A.counters + GART_CNT_BWD_TESTS, n_tests);
     count_add(A.counters + GART_CNT_BWD_ATOMICS, n_atom);
@@ -408,25 +410,29 @@ hipError_t launch_tk(const BackwardArgs& a, hipStream_t s) {
   constexpr int AS = acc_stride(K);
   const int n_tiles = a.tiles_x * a.tiles_y;
   hipError_t e = hipSuccess;
-  if (a.mode == GART_BACKWARD_GATHER) {
-    e = fill_u8(a.row_flag, 0, a.pair_count, s);
-    if (e != hipSuccess) return e;
-    if (n_tiles > 0) gather_kernel<TILE, K, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (a.n > 0) reduce_chain_kernel<K, true><<<ceil_div(a.n, 256), 256, 0, s>>>(a);
-    return hipGetLastError();
-  }
-  e = fill_f32(a.acc, 0.0f, a.n * AS, s);
+  const bool rows = a.mode == GART_BACKWARD_GATHER;
+  e = rows ? fill_u8(a.row_flag, 0, a.pair_count, s) : fill_f32(a.acc, 0.0f, a.n * AS, s);
   if (e != hipSuccess) return e;
+  if ((e = record(a.ev[0], s)) != hipSuccess) return e;
   if (n_tiles > 0) {
-    if (a.mode == GART_BACKWARD_GATHER_ATOMIC)
+    if (rows)
+      gather_kernel<TILE, K, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
+    else if (a.mode == GART_BACKWARD_GATHER_ATOMIC)
       gather_kernel<TILE, K, true><<<n_tiles, TILE * TILE, 0, s>>>(a);
     else
       scatter_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (a.n > 0) reduce_chain_kernel<K, false><<<ceil_div(a.n, 256), 256, 0, s>>>(a);
-  return hipGetLastError();
+  if ((e = record(a.ev[1], s)) != hipSuccess) return e;
+  if ((e = record(a.ev[2], s)) != hipSuccess) return e;
+  if (a.n > 0) {
+    if (rows)
+      reduce_chain_kernel<K, true><<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+    else
+      reduce_chain_kernel<K, false><<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return record(a.ev[3], s);
 }
 
 template <int TILE>

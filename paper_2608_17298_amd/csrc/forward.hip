@@ -267,8 +267,11 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
 template <int TILE, int K>
 hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
   const int n_tiles = a.tiles_x * a.tiles_y;
+  hipError_t e = record(a.ev_begin, s);
+  if (e != hipSuccess) return e;
   forward_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return record(a.ev_end, s);
 }
 
 template <int TILE>

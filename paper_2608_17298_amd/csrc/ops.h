@@ -26,6 +26,11 @@ size_t radix_tmp_bytes(int64_t m);
 hipError_t radix_sort_u32(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt, int64_t m, int bits,
                           void* tmp, hipStream_t s);
 
+// Records an optional event (no-op for NULL).
+inline hipError_t record(void* ev, hipStream_t s) {
+  return ev ? hipEventRecord(static_cast<hipEvent_t>(ev), s) : hipSuccess;
+}
+
 // Simple fills and gathers.
 hipError_t fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
 hipError_t fill_f32(float* p, float v, int64_t n, hipStream_t s);
@@ -85,6 +90,8 @@ struct ForwardArgs {
   float* image;
   gart_pixel_state* pixel_state;
   uint64_t* counters;
+  void* ev_begin;  // optional hipEvent_t recorded around the kernel
+  void* ev_end;
 };
 hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);
 
@@ -119,6 +126,7 @@ struct BackwardArgs {
   float* g_logits;
   float* g_sh;
   uint64_t* counters;
+  void* ev[4];  // optional hipEvent_t: main kernel begin/end, reduction begin/end
 };
 hipError_t launch_backward(const BackwardArgs& a, hipStream_t s);
 

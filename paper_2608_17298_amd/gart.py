@@ -35,8 +35,10 @@ SCATTER = 2
 MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER}
 
 CNT_FWD_HITS, CNT_FWD_TESTS, CNT_FWD_RESCANS = 0, 1, 2
-CNT_BWD_HITS, CNT_BWD_TESTS, CNT_BWD_ATOMICS, CNT_BWD_PAIRS = 3, 4, 5, 6
+CNT_BWD_HITS, CNT_BWD_TESTS, CNT_BWD_ATOMICS, CNT_BWD_PAIRS, CNT_BWD_ACTIVE = 3, 4, 5, 6, 7
 NUM_COUNTERS = 8
+EV_SORT, EV_FWD, EV_BWD, EV_REDUCE = 0, 2, 4, 6  # begin index; end = begin + 1
+NUM_EVENTS = 8
 
 _P = ctypes.c_void_p
 
@@ -62,7 +64,7 @@ class gart_frame(ctypes.Structure):
                 ("pair_offset", _P), ("pair_capacity", ctypes.c_int64), ("pair_tile", _P), ("pair_prim", _P),
                 ("tile_range", _P), ("lt_capacity", ctypes.c_int64), ("lt", _P), ("pixel_state", _P),
                 ("scratch", _P), ("scratch_bytes", ctypes.c_size_t), ("counters", _P),
-                ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
+                ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
                 ("stage", ctypes.c_int32)]
 
@@ -219,6 +221,7 @@ class Frame:
         self.pixel_state = torch.empty((camera.height * camera.width, 2), dtype=torch.int64, **dev)
         self.counters = torch.zeros(NUM_COUNTERS, dtype=torch.int64, **dev) if counters else None
         self.c = gart_frame()
+        self.events = [None] * NUM_EVENTS
         self.lt = self.pair_tile = self.pair_prim = self.scratch = None
         self._alloc_lt(lt_capacity)
         self._alloc_pairs(pair_capacity)
@@ -232,7 +235,11 @@ class Frame:
         self.pair_tile = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
         self.pair_prim = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
         self.pair_capacity = cap
-        nbytes = gart_scratch_bytes(self.n, self.sh_degree, cap, self.camera, self.settings)
+        # sized for every backward mode, so one frame serves all of them
+        nbytes = 0
+        for mode in (GATHER, GATHER_ATOMIC, SCATTER):
+            st = gart_settings(self.settings.alpha_min, self.settings.t_min, self.settings.tile, mode)
+            nbytes = max(nbytes, gart_scratch_bytes(self.n, self.sh_degree, cap, self.camera, st))
         self.scratch = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
 
     def grow(self, lt_entries: int, pair_count: int, slack: float = 1.0):
@@ -253,7 +260,14 @@ class Frame:
         f.lt, f.pixel_state = _ptr(self.lt), _ptr(self.pixel_state)
         f.scratch, f.scratch_bytes = _ptr(self.scratch), self.scratch.numel()
         f.counters = _ptr(self.counters)
+        for k in range(NUM_EVENTS):
+            f.events[k] = self.events[k]
         return f
+
+    def set_events(self, handles):
+        """Raw hipEvent_t handles (ints) the library records around its
+        kernels (see GART_EV_* in gart.h); None entries are not recorded."""
+        self.events = [None if h is None else int(h) for h in handles] + [None] * (NUM_EVENTS - len(handles))
 
     # host-side totals filled by the library
     @property
