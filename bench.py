@@ -299,7 +299,7 @@ def main():
         "forward_rescans": int(c[gart.CNT_FWD_RESCANS]),
         "counters": {name: int(c[i]) for i, name in enumerate(
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
-             "bwd_active_pairs"])},
+             "bwd_active_pairs", "fwd_drops"])},
         "kernels_roofline": {k: roofline(k) for k in work},
     }
     s = json.dumps(line)

@@ -147,7 +147,8 @@ enum {
   GART_CNT_BWD_ATOMICS = 5,   /* float atomic adds issued by the backward */
   GART_CNT_BWD_PAIRS = 6,     /* (tile, prim) pairs visited by the backward */
   GART_CNT_BWD_ACTIVE = 7,    /* visited pairs with at least one composited hit */
-  GART_NUM_COUNTERS = 8
+  GART_CNT_FWD_DROPS = 8,     /* forward hits dropped from a full hit buffer (found again by a rescan) */
+  GART_NUM_COUNTERS = 16
 };
 
 enum {

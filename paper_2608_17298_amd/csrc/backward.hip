@@ -321,61 +321,101 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 
 // ---------------------------------------------------------------------------
 // Per-Gaussian reduction of the pair rows (gather mode) or read of the
-// atomic accumulators, then the chain rule to the raw parameters.
+// atomic accumulators, then the chain rule to the raw parameters.  A block
+// serves 64 Gaussians.  Reduction: sixteen lanes per Gaussian, lane q reads
+// float4 q of each active row (rows are contiguous in emission order), 16
+// row flags are read at once and up to four rows are loaded per step.
+// Chain rule: one Gaussian per lane of the first wave.  SH gradients: all
+// threads, coalesced.
 // ---------------------------------------------------------------------------
-template <int K, bool ROWS>
-__global__ __launch_bounds__(256) void reduce_chain_kernel(BackwardArgs A) {
-  constexpr int AW = acc_width(K), AS = acc_stride(K);
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= A.n) return;
-  float acc[AW];
-#pragma unroll
-  for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
-  if constexpr (ROWS) {
-    const int64_t r0 = A.pair_offset[i], r1 = r0 + A.tile_count[i];
-    for (int64_t r = r0; r < r1; ++r) {
-      if (!A.row_flag[r]) continue;
-      const float4* src = reinterpret_cast<const float4*>(A.rows + r * AS);
-#pragma unroll
-      for (int v = 0; v < AS; v += 4) {
-        const float4 q = src[v / 4];
-        if (v + 0 < AW) acc[v + 0] += q.x;
-        if (v + 1 < AW) acc[v + 1] += q.y;
-        if (v + 2 < AW) acc[v + 2] += q.z;
-        if (v + 3 < AW) acc[v + 3] += q.w;
-      }
-    }
-  } else {
-    const float* src = A.acc + i * AS;
-#pragma unroll
-    for (int v = 0; v < AW; ++v) acc[v] = src[v];
-  }
+constexpr int kReduceLanes = 16;
+constexpr int kReduceBlock = 256;
+constexpr int kReduceGaussians = 64;
 
+template <int K, bool ROWS>
+__global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs A) {
+  constexpr int AS = acc_stride(K), NQ = AS / 4;
+  constexpr int GROUPS = kReduceBlock / kReduceLanes;
+  static_assert(NQ <= kReduceLanes, "accumulator row wider than a lane group");
+  __shared__ __align__(16) float s_acc[kReduceGaussians][AS];
+  const int64_t i0 = int64_t(blockIdx.x) * kReduceGaussians;
+  const int grp = threadIdx.x / kReduceLanes, q = threadIdx.x % kReduceLanes;
+  const int shift = (threadIdx.x % 64) / kReduceLanes * kReduceLanes;
+
+  for (int gl = grp; gl < kReduceGaussians; gl += GROUPS) {
+    const int64_t i = i0 + gl;
+    const bool live = i < A.n;
+    const uint32_t tc = live ? A.tile_count[i] : 0u;
+    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if constexpr (ROWS) {
+      const float4* rows = reinterpret_cast<const float4*>(A.rows);
+      const int64_t r0 = live ? A.pair_offset[i] : 0, r1 = r0 + tc;
+      for (int64_t rb = r0; rb < r1; rb += kReduceLanes) {
+        const int64_t rq = rb + q;
+        const bool act = rq < r1 && A.row_flag[rq] != 0;
+        uint32_t m = uint32_t(__ballot(act) >> shift) & 0xffffu;
+        while (m) {
+          int k[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            k[u] = m ? __ffs(m) - 1 : -1;
+            m &= m ? m - 1 : 0u;
+          }
+          float4 v[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            v[u] = (k[u] >= 0 && q < NQ) ? rows[(rb + k[u]) * NQ + q] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            a.x += v[u].x;
+            a.y += v[u].y;
+            a.z += v[u].z;
+            a.w += v[u].w;
+          }
+        }
+      }
+    } else if (live && tc && q < NQ) {
+      a = reinterpret_cast<const float4*>(A.acc)[i * NQ + q];
+    }
+    if (q < NQ) reinterpret_cast<float4*>(s_acc[gl])[q] = a;
+  }
+  __syncthreads();
+
+  const int nb = int(min<int64_t>(kReduceGaussians, A.n - i0));
+  for (int e = threadIdx.x; e < nb * 3 * K; e += kReduceBlock) {
+    const int gl = e / (3 * K), v = e % (3 * K);
+    A.g_sh[(i0 + gl) * 3 * K + v] = s_acc[gl][10 + v];
+  }
+  if (int(threadIdx.x) >= nb) return;
+  const int64_t i = i0 + threadIdx.x;
+  const float* acc = s_acc[threadIdx.x];
   float* gm = A.g_means + 3 * i;
   float* gs = A.g_log_scales + 3 * i;
   float* gq = A.g_quats + 4 * i;
-  float* gsh = A.g_sh + i * 3 * K;
-  if (A.tile_count[i] == 0) {  // culled: no ray can reach it
+  if (A.tile_count[i] == 0) {  // culled: no ray can reach it (its sums are zero)
     for (int k = 0; k < 3; ++k) gm[k] = gs[k] = 0.0f;
     for (int k = 0; k < 4; ++k) gq[k] = 0.0f;
     A.g_logits[i] = 0.0f;
-    for (int k = 0; k < 3 * K; ++k) gsh[k] = 0.0f;
     return;
   }
   const double qw0 = A.quats[4 * i], qx0 = A.quats[4 * i + 1], qy0 = A.quats[4 * i + 2], qz0 = A.quats[4 * i + 3];
-  const double qn = sqrt(qw0 * qw0 + qx0 * qx0 + qy0 * qy0 + qz0 * qz0);
-  const double w = qw0 / qn, x = qx0 / qn, y = qy0 / qn, z = qz0 / qn;
+  const double inv_qn = 1.0 / sqrt(qw0 * qw0 + qx0 * qx0 + qy0 * qy0 + qz0 * qz0);
+  const double w = qw0 * inv_qn, x = qx0 * inv_qn, y = qy0 * inv_qn, z = qz0 * inv_qn;
   const double R[3][3] = {{1.0 - 2.0 * (y * y + z * z), 2.0 * (x * y - w * z), 2.0 * (x * z + w * y)},
                           {2.0 * (x * y + w * z), 1.0 - 2.0 * (x * x + z * z), 2.0 * (y * z - w * x)},
                           {2.0 * (x * z - w * y), 2.0 * (y * z + w * x), 1.0 - 2.0 * (x * x + y * y)}};
-  const double s[3] = {exp(double(A.log_scales[3 * i])), exp(double(A.log_scales[3 * i + 1])),
-                       exp(double(A.log_scales[3 * i + 2]))};
+  double s[3], is[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    s[k] = exp(double(A.log_scales[3 * i + k]));
+    is[k] = 1.0 / s[k];
+  }
   const double go[3] = {acc[0], acc[1], acc[2]};
   const double B[3][3] = {{acc[3], acc[6], acc[7]}, {acc[6], acc[4], acc[8]}, {acc[7], acc[8], acc[5]}};
   // dL/dmu = -R S^-1 go
 #pragma unroll
   for (int j = 0; j < 3; ++j)
-    gm[j] = float(-(R[j][0] * go[0] / s[0] + R[j][1] * go[1] / s[1] + R[j][2] * go[2] / s[2]));
+    gm[j] = float(-(R[j][0] * go[0] * is[0] + R[j][1] * go[1] * is[1] + R[j][2] * go[2] * is[2]));
   // dL/dlog s_k = -B_kk
 #pragma unroll
   for (int k = 0; k < 3; ++k) gs[k] = float(-B[k][k]);
@@ -385,7 +425,7 @@ __global__ __launch_bounds__(256) void reduce_chain_kernel(BackwardArgs A) {
   for (int j = 0; j < 3; ++j)
 #pragma unroll
     for (int k = 0; k < 3; ++k)
-      GR[j][k] = (R[j][0] * s[0] * B[0][k] + R[j][1] * s[1] * B[1][k] + R[j][2] * s[2] * B[2][k]) / s[k];
+      GR[j][k] = (R[j][0] * s[0] * B[0][k] + R[j][1] * s[1] * B[1][k] + R[j][2] * s[2] * B[2][k]) * is[k];
   // dL/d(unit quaternion), then through q / |q|
   double dq[4];
   dq[0] = 2.0 * (z * (GR[1][0] - GR[0][1]) + y * (GR[0][2] - GR[2][0]) + x * (GR[2][1] - GR[1][2]));
@@ -398,11 +438,9 @@ __global__ __launch_bounds__(256) void reduce_chain_kernel(BackwardArgs A) {
   const double proj = w * dq[0] + x * dq[1] + y * dq[2] + z * dq[3];
   const double qv[4] = {w, x, y, z};
 #pragma unroll
-  for (int k = 0; k < 4; ++k) gq[k] = float((dq[k] - qv[k] * proj) / qn);
+  for (int k = 0; k < 4; ++k) gq[k] = float((dq[k] - qv[k] * proj) * inv_qn);
   const double sig = A.geom[int64_t(kGeomStride) * i + kGeoSigma];
   A.g_logits[i] = float(sig * (1.0 - sig) * double(acc[9]));
-#pragma unroll
-  for (int k = 0; k < 3 * K; ++k) gsh[k] = acc[10 + k];
 }
 
 template <int TILE, int K>
@@ -426,10 +464,11 @@ hipError_t launch_tk(const BackwardArgs& a, hipStream_t s) {
   if ((e = record(a.ev[1], s)) != hipSuccess) return e;
   if ((e = record(a.ev[2], s)) != hipSuccess) return e;
   if (a.n > 0) {
+    const int64_t blocks = ceil_div(a.n, kReduceGaussians);
     if (rows)
-      reduce_chain_kernel<K, true><<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+      reduce_chain_kernel<K, true><<<blocks, kReduceBlock, 0, s>>>(a);
     else
-      reduce_chain_kernel<K, false><<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+      reduce_chain_kernel<K, false><<<blocks, kReduceBlock, 0, s>>>(a);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(a.ev[3], s);

@@ -148,11 +148,34 @@ __global__ __launch_bounds__(256) void bounds_kernel(BoundsArgs A) {
         }
         G[kGeoD2c] = D2c;
         G[kGeoSigma] = sigma;
-        // Any hit point lies inside the ball of radius alpha_c max(s) around
-        // mu, so its depth along the unit ray is at least |mu - o| - r.
+        // Lower bound on the depth tau of any hit.  The max-response point
+        // x = o + tau d lies in the clamped ellipsoid, hence within r =
+        // alpha_c max(s) of mu, so tau >= |mu - o| - r.  Tighter: x is the
+        // midpoint of the ray's chord, so y = x - mu lies on the diametral
+        // plane conjugate to d (y^T Sigma^-1 d = 0) with y^T Sigma^-1 y <=
+        // alpha_c^2, which gives |y.d| <= alpha_c sqrt(d^T Sigma d -
+        // 1/(d^T Sigma^-1 d)); and (mu - o).d >= sqrt(|mu-o|^2 - r^2) since
+        // the ray passes within r of mu.  Over directions d within the angle
+        // th = asin(r/|mu-o|) of u = (mu - o)/|mu - o|:
+        //   |S R^T d| <= |S R^T u| + s_max th,  |S^-1 R^T d| <= |S^-1 R^T u| + th / s_min.
         const double dist = sqrt(om[0] * om[0] + om[1] * om[1] + om[2] * om[2]);
-        const double r = ac * fmax(s[0], fmax(s[1], s[2]));
-        const double lo = dist - r - 1e-12 * (dist + r);
+        const double smax = fmax(s[0], fmax(s[1], s[2])), smin = fmin(s[0], fmin(s[1], s[2]));
+        const double r = ac * smax;
+        double lo = dist - r;
+        if (dist > r) {
+          const double th = asin(r / dist);
+          double a1 = 0.0, a2 = 0.0;
+#pragma unroll
+          for (int k = 0; k < 3; ++k) {
+            const double ck = -(R[k] * om[0] + R[3 + k] * om[1] + R[6 + k] * om[2]) / dist;  // (R^T u)_k
+            a1 += ck * ck * s[k] * s[k];
+            a2 += ck * ck / (s[k] * s[k]);
+          }
+          const double p = sqrt(a1) + smax * th, q = sqrt(a2) + th / smin;
+          const double hb = sqrt(fmax(0.0, p * p - 1.0 / (q * q)));
+          lo = fmax(lo, sqrt(dist * dist - r * r) - ac * hb);
+        }
+        lo -= 1e-12 * (dist + r);
         key = lo > 0.0 ? __double2float_rd(lo) : 0.0f;
         G[kGeoKey] = double(key);
         const int ts = A.tile;

@@ -20,6 +20,10 @@
 namespace gart {
 namespace {
 
+#ifndef GART_FWD_KB
+#define GART_FWD_KB 12
+#endif
+
 constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
 // Each rescan composites at least one hit per rescanning lane, so the pass
 // count is bounded by the hits of a tile; this cap only guards against a
@@ -31,7 +35,7 @@ constexpr int kMaxPasses = 1 << 20;
 template <int TILE, int K>
 __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int NT = TILE * TILE;
-  constexpr int KB = 8;  // per-lane hit buffer (registers)
+  constexpr int KB = GART_FWD_KB;  // per-lane hit buffer (registers)
   constexpr double kInf = __builtin_huge_val();
 
   __shared__ __align__(16) double s_row[NT * kRow];
@@ -56,7 +60,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   bool done = !valid;     // terminated (or no pixel)
   bool finished = false;  // every hit composited
   bool stalled = false;   // must wait for a rescan
-  uint32_t n_hits = 0, n_tests = 0;
+  uint32_t n_hits = 0, n_tests = 0, n_drops = 0;
   double last_tau = -kInf;
   uint32_t last_id = 0;
   double end_tau = kInf;
@@ -79,6 +83,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   }
 
   auto drop = [&](double t, uint32_t id, uint32_t c) {
+    ++n_drops;
     if (key_less(t, id, e_tau, e_id)) {
       e_tau = t;
       e_id = id;
@@ -259,6 +264,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   if (A.counters) {
     count_add(A.counters + GART_CNT_FWD_HITS, n_hits);
     count_add(A.counters + GART_CNT_FWD_TESTS, n_tests);
+    count_add(A.counters + GART_CNT_FWD_DROPS, n_drops);
     if (tid == 0 && passes)
       atomicAdd(reinterpret_cast<unsigned long long*>(A.counters + GART_CNT_FWD_RESCANS), (unsigned long long)passes);
   }

@@ -36,7 +36,8 @@ MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER}
 
 CNT_FWD_HITS, CNT_FWD_TESTS, CNT_FWD_RESCANS = 0, 1, 2
 CNT_BWD_HITS, CNT_BWD_TESTS, CNT_BWD_ATOMICS, CNT_BWD_PAIRS, CNT_BWD_ACTIVE = 3, 4, 5, 6, 7
-NUM_COUNTERS = 8
+CNT_FWD_DROPS = 8
+NUM_COUNTERS = 16
 EV_SORT, EV_FWD, EV_BWD, EV_REDUCE = 0, 2, 4, 6  # begin index; end = begin + 1
 NUM_EVENTS = 8
 
