@@ -29,11 +29,12 @@ constexpr int kRow = 20;  // doubles per staged Gaussian (same layout as the for
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Gradient contribution of one composited hit, in the accumulator layout.
+// Adds the gradient contribution of one composited hit to acc (accumulator
+// layout), with explicit fused multiply-adds.
 template <int K>
-__device__ __forceinline__ void hit_grad(double D2, const double xg[3], double sigma, const float sh[3 * K],
-                                         const float Y[K], const float C[3], const float g[3], float4 lt,
-                                         float out[acc_width(K)]) {
+__device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], double sigma, const float sh[3 * K],
+                                             const float Y[K], const float C[3], const float g[3], float4 lt,
+                                             float acc[acc_width(K)]) {
   const float rho = expf(float(-0.5 * D2));
   const float a = float(sigma) * rho;
   float c[3];
@@ -54,46 +55,60 @@ __device__ __forceinline__ void hit_grad(double D2, const double xg[3], double s
   float dc[3];
 #pragma unroll
   for (int ch = 0; ch < 3; ++ch) {
-    const float S = C[ch] - Lc[ch] - ta * c[ch];
-    dlda = fmaf(g[ch], T * c[ch] - S * inv, dlda);
+    const float S = fmaf(-ta, c[ch], C[ch] - Lc[ch]);  // colour behind the hit
+    dlda = fmaf(g[ch], fmaf(T, c[ch], -S * inv), dlda);
     dc[ch] = pos[ch] ? ta * g[ch] : 0.0f;
   }
   const float u2 = -a * dlda;
   const float x = float(xg[0]), y = float(xg[1]), z = float(xg[2]);
-  out[0] = u2 * x;
-  out[1] = u2 * y;
-  out[2] = u2 * z;
-  out[3] = u2 * x * x;
-  out[4] = u2 * y * y;
-  out[5] = u2 * z * z;
-  out[6] = u2 * x * y;
-  out[7] = u2 * x * z;
-  out[8] = u2 * y * z;
-  out[9] = dlda * rho;
+  const float ux = u2 * x, uy = u2 * y, uz = u2 * z;
+  acc[0] += ux;
+  acc[1] += uy;
+  acc[2] += uz;
+  acc[3] = fmaf(ux, x, acc[3]);
+  acc[4] = fmaf(uy, y, acc[4]);
+  acc[5] = fmaf(uz, z, acc[5]);
+  acc[6] = fmaf(ux, y, acc[6]);
+  acc[7] = fmaf(ux, z, acc[7]);
+  acc[8] = fmaf(uy, z, acc[8]);
+  acc[9] = fmaf(dlda, rho, acc[9]);
 #pragma unroll
   for (int k = 0; k < K; ++k)
 #pragma unroll
-    for (int ch = 0; ch < 3; ++ch) out[10 + 3 * k + ch] = dc[ch] * Y[k];
+    for (int ch = 0; ch < 3; ++ch) acc[10 + 3 * k + ch] = fmaf(dc[ch], Y[k], acc[10 + 3 * k + ch]);
 }
 
 // ---------------------------------------------------------------------------
-// Gather: one workgroup per tile; lane j owns pairs j, j+NT, ... of the
-// tile's list (ordered by depth lower bound).  Per pixel state is staged in
-// LDS once per tile.
+// Gather: one workgroup per tile; each lane owns whole (tile, Gaussian)
+// pairs.  Per-pixel state (ray direction, end marker, SH basis, colour and
+// upstream gradient) is staged in LDS once per tile, pixel-major so a lane
+// reads one pixel's fields with 128-bit loads.  Only pairs whose depth bound
+// lies in front of the tile's last ray end are visited (a prefix of the
+// depth-ordered list).  Visited pairs are dealt to lanes largest first
+// (counting sort by pixel count in LDS) so that lanes working in the same
+// round have similar loads.  Each pair first tests its pixels into a
+// bit mask of composited hits, then accumulates the gradient of those hits
+// in registers, and finally writes one partial row (or adds it atomically).
 // ---------------------------------------------------------------------------
+constexpr int kSortChunk = 2048;  // visited pairs ordered per LDS pass
+
 template <int TILE, int K, bool ATOMIC>
 __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   constexpr int NT = TILE * TILE;
+  constexpr int kChunkRows = 64 / TILE;  // rows of a tile whose pixels fit one 64-bit mask
   constexpr int AW = acc_width(K), AS = acc_stride(K);
+  constexpr int KP = (K + 3) & ~3;       // SH basis row padded to 16 bytes
   constexpr double kInf = __builtin_huge_val();
 
-  __shared__ double s_d[3][NT];
-  __shared__ float s_Y[K][NT];
-  __shared__ float s_C[3][NT];
-  __shared__ float s_g[3][NT];
-  __shared__ double s_tend[NT];
+  __shared__ double4 s_ray[NT];                 // d.xyz, tau_end
   __shared__ uint32_t s_iend[NT];
+  __shared__ __align__(16) float s_Y[NT][KP];
+  __shared__ __align__(16) float s_cg[NT][8];   // C.rgb, g.rgb
   __shared__ double s_wmax[NT / 64];
+  __shared__ uint32_t s_red[NT / 64];
+  __shared__ uint32_t s_hist[64];
+  __shared__ uint8_t s_bucket[kSortChunk];
+  __shared__ uint16_t s_order[kSortChunk];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
   const int tile = xcd_tile(blockIdx.x, n_tiles);
@@ -109,27 +124,25 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     float Y[K];
     sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
 #pragma unroll
-    for (int k = 0; k < 3; ++k) s_d[k][tid] = d[k];
-#pragma unroll
-    for (int k = 0; k < K; ++k) s_Y[k][tid] = Y[k];
+    for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
     double tend = -kInf;
     uint32_t iend = 0;
+    float cg[6] = {0, 0, 0, 0, 0, 0};
     if (valid) {
       const int64_t p = int64_t(py) * A.cam.W + px;
 #pragma unroll
       for (int ch = 0; ch < 3; ++ch) {
-        s_C[ch][tid] = A.image[3 * p + ch];
-        s_g[ch][tid] = A.dl_dimage[3 * p + ch];
+        cg[ch] = A.image[3 * p + ch];
+        cg[3 + ch] = A.dl_dimage[3 * p + ch];
       }
       const gart_pixel_state st = A.pixel_state[p];
       tend = st.tau_end;
       iend = st.id_end;
-    } else {
-#pragma unroll
-      for (int ch = 0; ch < 3; ++ch) s_C[ch][tid] = s_g[ch][tid] = 0.0f;
     }
-    s_tend[tid] = tend;
+    s_ray[tid] = make_double4(d[0], d[1], d[2], tend);
     s_iend[tid] = iend;
+    *reinterpret_cast<float4*>(&s_cg[tid][0]) = make_float4(cg[0], cg[1], cg[2], cg[3]);
+    *reinterpret_cast<float4*>(&s_cg[tid][4]) = make_float4(cg[4], cg[5], 0.0f, 0.0f);
     double m = tend;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
@@ -140,74 +153,153 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
 #pragma unroll
   for (int w = 1; w < NT / 64; ++w) tmax = fmax(tmax, s_wmax[w]);
 
+  // Number of visited pairs: the list is ordered by depth bound, so they
+  // form its prefix of pairs whose bound is <= tmax.
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
-  uint32_t n_pairs = 0, n_hits = 0, n_tests = 0, n_atom = 0, n_active = 0;
+  uint32_t nv = 0;
   for (int64_t j = beg + tid; j < end; j += NT) {
-    const uint32_t i = A.pair_prim[j];
-    const double* G = A.geom + int64_t(kGeomStride) * i;
-    if (G[kGeoKey] > tmax) break;  // this and every later pair lie behind every ray's end
-    ++n_pairs;
-    double W[9], og[3];
+    if (A.geom[int64_t(kGeomStride) * A.pair_prim[j] + kGeoKey] > tmax) break;
+    ++nv;
+  }
 #pragma unroll
-    for (int k = 0; k < 9; ++k) W[k] = G[k];
+  for (int off = 32; off > 0; off >>= 1) nv += __shfl_xor(nv, off);
+  if (__lane_id() == 0) s_red[tid / 64] = nv;
+  __syncthreads();
+  int64_t V = 0;
 #pragma unroll
-    for (int k = 0; k < 3; ++k) og[k] = G[kGeoOg + k];
-    const double D2c = G[kGeoD2c], sigma = G[kGeoSigma];
-    const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
-    float sh[3 * K];
-    const float* shp = A.sh + int64_t(i) * (3 * K);
-#pragma unroll
-    for (int k = 0; k < 3 * K; ++k) sh[k] = shp[k];
-    const int xa = max(r.x, ox), xb = min(r.z, ox + TILE - 1);
-    const int ya = max(r.y, oy), yb = min(r.w, oy + TILE - 1);
-    int64_t idx = A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, xa, ya);
-    float acc[AW];
-#pragma unroll
-    for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
-    bool any = false;
-    for (int y = ya; y <= yb; ++y) {
-      for (int x = xa; x <= xb; ++x, ++idx) {
-        const int lp = (y - oy) * TILE + (x - ox);
-        const double d[3] = {s_d[0][lp], s_d[1][lp], s_d[2][lp]};
-        double tau, D2, xg[3];
-        ++n_tests;
-        if (!ray_hit(W, og, D2c, d, &tau, &D2, xg)) continue;
-        if (key_less(s_tend[lp], s_iend[lp], tau, i)) continue;  // behind the ray's last composited hit
-        ++n_hits;
-        any = true;
-        const float4 lt = A.lt[idx];
-        float Y[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) Y[k] = s_Y[k][lp];
-        const float C[3] = {s_C[0][lp], s_C[1][lp], s_C[2][lp]};
-        const float g[3] = {s_g[0][lp], s_g[1][lp], s_g[2][lp]};
-        float h[AW];
-        hit_grad<K>(D2, xg, sigma, sh, Y, C, g, lt, h);
-#pragma unroll
-        for (int v = 0; v < AW; ++v) acc[v] += h[v];
-      }
+  for (int w = 0; w < NT / 64; ++w) V += s_red[w];
+
+  uint32_t n_pairs = 0, n_hits = 0, n_tests = 0, n_atom = 0, n_active = 0;
+  for (int64_t c0 = 0; c0 < V; c0 += kSortChunk) {
+    const int nc = int(min<int64_t>(kSortChunk, V - c0));
+    __syncthreads();  // the previous chunk's order is no longer read
+    if (tid < 64) s_hist[tid] = 0;
+    __syncthreads();
+    for (int q = tid; q < nc; q += NT) {
+      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(A.pair_prim[beg + c0 + q]));
+      const int npx = (min(r.z, ox + TILE - 1) - max(r.x, ox) + 1) * (min(r.w, oy + TILE - 1) - max(r.y, oy) + 1);
+      const int bk = 63 - min(63, (npx - 1) * 64 / NT);  // larger footprints first
+      s_bucket[q] = uint8_t(bk);
+      atomicAdd(&s_hist[bk], 1u);
     }
-    if (!any) continue;
-    ++n_active;
-    if constexpr (ATOMIC) {
-      float* dst = A.acc + int64_t(i) * AS;
+    __syncthreads();
+    if (tid < 64) {  // exclusive scan of the 64 bucket counts (one wave)
+      const uint32_t c = s_hist[tid];
+      uint32_t inc = c;
 #pragma unroll
-      for (int v = 0; v < AW; ++v) unsafeAtomicAdd(dst + v, acc[v]);
-      n_atom += AW;
-    } else {
-      const int tx0 = r.x / TILE, ty0 = r.y / TILE, tx1 = r.z / TILE;
-      const int64_t row = A.pair_offset[i] + int64_t(ty - ty0) * (tx1 - tx0 + 1) + (tx - tx0);
-      float4* dst = reinterpret_cast<float4*>(A.rows + row * AS);
-#pragma unroll
-      for (int v = 0; v < AS; v += 4) {
-        float4 q;
-        q.x = v + 0 < AW ? acc[v + 0] : 0.0f;
-        q.y = v + 1 < AW ? acc[v + 1] : 0.0f;
-        q.z = v + 2 < AW ? acc[v + 2] : 0.0f;
-        q.w = v + 3 < AW ? acc[v + 3] : 0.0f;
-        dst[v / 4] = q;
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t u = __shfl_up(inc, off);
+        if (__lane_id() >= unsigned(off)) inc += u;
       }
-      A.row_flag[row] = 1;
+      s_hist[tid] = inc - c;
+    }
+    __syncthreads();
+    for (int q = tid; q < nc; q += NT) s_order[atomicAdd(&s_hist[s_bucket[q]], 1u)] = uint16_t(q);
+    __syncthreads();
+
+    for (int q = tid; q < nc; q += NT) {
+      const int64_t j = beg + c0 + s_order[q];
+      const uint32_t i = A.pair_prim[j];
+      const double* G = A.geom + int64_t(kGeomStride) * i;
+      ++n_pairs;
+      double W[9], og[3];
+#pragma unroll
+      for (int k = 0; k < 9; ++k) W[k] = G[k];
+#pragma unroll
+      for (int k = 0; k < 3; ++k) og[k] = G[kGeoOg + k];
+      const double D2c = G[kGeoD2c], sigma = G[kGeoSigma], key = G[kGeoKey];
+      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
+      float sh[3 * K];
+      const float* shp = A.sh + int64_t(i) * (3 * K);
+#pragma unroll
+      for (int k = 0; k < 3 * K; ++k) sh[k] = shp[k];
+      const int xa = max(r.x, ox), xb = min(r.z, ox + TILE - 1);
+      const int ya = max(r.y, oy), yb = min(r.w, oy + TILE - 1);
+      const int64_t base = A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, xa, ya);
+      const int w = xb - xa + 1;
+      float acc[AW];
+#pragma unroll
+      for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
+      bool any = false;
+      // Rows of rect cap tile in chunks of at most 64 pixels.
+      for (int y0 = ya; y0 <= yb; y0 += kChunkRows) {
+        const int y1 = min(yb, y0 + kChunkRows - 1);
+        const int lp0 = (y0 - oy) * TILE;
+        // Phase 1: which pixels hold a composited hit of this Gaussian (bit =
+        // pixel index within the chunk).  A pixel whose ray ended in front of
+        // the Gaussian's depth bound is skipped without a test.
+        uint64_t mask = 0;
+        for (int y = y0; y <= y1; ++y) {
+          for (int x = xa; x <= xb; ++x) {
+            const int b = (y - y0) * TILE + (x - ox);
+            const double4 ry = s_ray[lp0 + b];
+            if (key > ry.w) continue;
+            const double d[3] = {ry.x, ry.y, ry.z};
+            double tau, D2, xg[3];
+            ++n_tests;
+            if (ray_hit(W, og, D2c, d, &tau, &D2, xg) && !key_less(ry.w, s_iend[lp0 + b], tau, i))
+              mask |= 1ull << b;
+          }
+        }
+        if (!mask) continue;
+        any = true;
+        // Phase 2: the gradient of each composited hit, in row-major order.
+        // (L,T) index: base + row offset within rect cap tile + column offset.
+        auto lt_at = [&](int b) {
+          return A.lt[base + int64_t(y0 - ya + b / TILE) * w + (b % TILE - (xa - ox))];
+        };
+        int b = __builtin_ctzll(mask);
+        float4 lt_next = lt_at(b);
+        while (mask) {
+          const float4 lt = lt_next;
+          mask &= mask - 1;
+          const int bn = mask ? __builtin_ctzll(mask) : b;
+          if (mask) lt_next = lt_at(bn);
+          const int lp = lp0 + b;
+          const double4 ry = s_ray[lp];
+          const double d[3] = {ry.x, ry.y, ry.z};
+          double tau, D2, xg[3];
+          ray_hit(W, og, D2c, d, &tau, &D2, xg);
+          ++n_hits;
+          float Y[KP];
+#pragma unroll
+          for (int kk = 0; kk < KP; kk += 4) {
+            const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[lp][kk]);
+            Y[kk] = y4.x;
+            Y[kk + 1] = y4.y;
+            Y[kk + 2] = y4.z;
+            Y[kk + 3] = y4.w;
+          }
+          const float4 c4 = *reinterpret_cast<const float4*>(&s_cg[lp][0]);
+          const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
+          const float C[3] = {c4.x, c4.y, c4.z};
+          const float g[3] = {c4.w, g4.x, g4.y};
+          hit_grad_acc<K>(D2, xg, sigma, sh, Y, C, g, lt, acc);
+          b = bn;
+        }
+      }
+      if (!any) continue;
+      ++n_active;
+      if constexpr (ATOMIC) {
+        float* dst = A.acc + int64_t(i) * AS;
+#pragma unroll
+        for (int v = 0; v < AW; ++v) unsafeAtomicAdd(dst + v, acc[v]);
+        n_atom += AW;
+      } else {
+        const int tx0 = r.x / TILE, ty0 = r.y / TILE, tx1 = r.z / TILE;
+        const int64_t row = A.pair_offset[i] + int64_t(ty - ty0) * (tx1 - tx0 + 1) + (tx - tx0);
+        float4* dst = reinterpret_cast<float4*>(A.rows + row * AS);
+#pragma unroll
+        for (int v = 0; v < AS; v += 4) {
+          float4 q4;
+          q4.x = v + 0 < AW ? acc[v + 0] : 0.0f;
+          q4.y = v + 1 < AW ? acc[v + 1] : 0.0f;
+          q4.z = v + 2 < AW ? acc[v + 2] : 0.0f;
+          q4.w = v + 3 < AW ? acc[v + 3] : 0.0f;
+          dst[v / 4] = q4;
+        }
+        A.row_flag[row] = 1;
+      }
     }
   }
   if (A.counters) {
@@ -303,7 +395,9 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 #pragma unroll
         for (int k = 0; k < 3 * K; ++k) sh[k] = shp[k];
         float h[AW];
-        hit_grad<K>(D2, xg, row[13], sh, Y, C, g, lt, h);
+#pragma unroll
+        for (int v = 0; v < AW; ++v) h[v] = 0.0f;
+        hit_grad_acc<K>(D2, xg, row[13], sh, Y, C, g, lt, h);
         float* dst = A.acc + int64_t(id) * AS;
 #pragma unroll
         for (int v = 0; v < AW; ++v) unsafeAtomicAdd(dst + v, h[v]);

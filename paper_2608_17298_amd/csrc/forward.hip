@@ -23,6 +23,9 @@ namespace {
 #ifndef GART_FWD_KB
 #define GART_FWD_KB 12
 #endif
+#ifndef GART_FWD_FLUSH
+#define GART_FWD_FLUSH 4
+#endif
 
 constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
 // Each rescan composites at least one hit per rescanning lane, so the pass
@@ -36,6 +39,7 @@ template <int TILE, int K>
 __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int NT = TILE * TILE;
   constexpr int KB = GART_FWD_KB;  // per-lane hit buffer (registers)
+  constexpr int kFlushEvery = GART_FWD_FLUSH;
   constexpr double kInf = __builtin_huge_val();
 
   __shared__ __align__(16) double s_row[NT * kRow];
@@ -215,12 +219,17 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
               }
             }
           }
-          const double nk = double(s_key[c + 1]);
-          while (cnt > 0 && bt[0] < nk && !done) composite_front();
-          if (done) break;
-          if (e_tau < kInf && nk > e_tau) {
-            stalled = true;
-            break;
+          // Composite the final hits every kFlushEvery Gaussians (so that each
+          // compositing step serves more lanes), at the end of a batch, and
+          // whenever the buffer is full.
+          if ((c + 1) % kFlushEvery == 0 || c + 1 == nb || cnt == KB) {
+            const double nk = double(s_key[c + 1]);
+            while (cnt > 0 && bt[0] < nk && !done) composite_front();
+            if (done) break;
+            if (e_tau < kInf && nk > e_tau) {
+              stalled = true;
+              break;
+            }
           }
         }
       }
