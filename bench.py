@@ -154,7 +154,7 @@ def main():
         gart.gart_bounds(g, cam, stm, frame)
         gart.gart_build_tile_map(cam, stm, frame)
         gart.gart_forward(g, cam, stm, frame, image)
-        gart.gart_backward(g, cam, stm, frame, image, dl, grads)
+        gart.gart_backward(g, cam, stm, frame, dl, grads)
         torch.cuda.synchronize()
         counts[mode] = frame.counters.cpu().numpy().astype(np.int64)
     frame.counters = None
@@ -189,7 +189,7 @@ def main():
                 gart.gart_forward(g, cam, settings, frame, image)
             if timed:
                 call[3].record(stream)
-            gart.gart_backward(g, cam, settings, frame, image, dl, grads)
+            gart.gart_backward(g, cam, settings, frame, dl, grads)
             if timed:
                 call[4].record(stream)
                 per.append((call, kern))
@@ -228,10 +228,10 @@ def main():
     fwd_tests = int(c[gart.CNT_FWD_TESTS])
     work = {
         "backward_main": dict(
-            bytes=16 * bwd_hits + bwd_pairs * (GEOM_BYTES + 12 * K) + bwd_active * (4 * AS + 1) + npix * (12 + 12 + 16),
+            bytes=16 * bwd_hits + bwd_pairs * (GEOM_BYTES + 12 * K) + bwd_active * (4 * AS + 1) + npix * (12 + 32),
             f64=F64_PER_TEST * bwd_tests, f32=f32_per_hit_bwd(K) * bwd_hits),
         "forward_trace": dict(
-            bytes=16 * hits + int(frame.pair_count) * GEOM_BYTES + npix * (12 + 16) + hits * 12 * K,
+            bytes=16 * hits + int(frame.pair_count) * GEOM_BYTES + npix * (12 + 32) + hits * 12 * K,
             f64=F64_PER_TEST * fwd_tests + 30 * hits, f32=f32_per_hit_fwd(K) * hits),
     }
 

@@ -91,15 +91,30 @@ typedef struct {
   int32_t backward_mode;  /* gart_backward_mode */
 } gart_settings;
 
-/* Per-pixel state the forward leaves for the backward (16 bytes): the depth
+/* Per-pixel state the forward leaves for the backward (32 bytes): the depth
  * and index of the last composited hit if the ray terminated (T < t_min),
  * else tau_end = +inf and id_end = 0xffffffff; a hit (tau, i) of this pixel
- * was composited iff (tau, i) <= (tau_end, id_end) lexicographically. */
+ * was composited iff (tau, i) <= (tau_end, id_end) lexicographically.
+ * color_fixed is the final pixel colour C (Eq. 1) in the fixed point of
+ * gart_lt_entry, so that the colour behind a hit, C - L - T a c, is formed
+ * from an exact integer difference C - L. */
 typedef struct {
   double tau_end;
   uint32_t id_end;
-  uint32_t n_hits;        /* composited hits of the pixel */
+  uint32_t n_hits;          /* composited hits of the pixel */
+  uint32_t color_fixed[3];  /* round(C / gart_frame.color_step) per channel */
+  float t_final;            /* transmittance left after the last composited hit */
 } gart_pixel_state;
+
+/* One intermediate-buffer entry (Sec. 4.3, 16 bytes): the colour
+ * accumulated in front of a composited hit, L, as unsigned fixed point
+ * (L = L_fixed * gart_frame.color_step, rounded to nearest; every composited
+ * colour lies below 2^32 color_step), and the transmittance T in front of
+ * the hit. */
+typedef struct {
+  uint32_t L_fixed[3];
+  float T;
+} gart_lt_entry;
 
 /* Per-frame buffers.  Host struct; the caller allocates every device array
  * (sizes in the comments; "cap" = the capacity fields) and the library
@@ -118,7 +133,7 @@ typedef struct {
   int64_t* tile_range;    /* [n_tiles+1] pairs of tile t are [tile_range[t], tile_range[t+1]) */
   /* written by gart_forward, read by gart_backward */
   int64_t lt_capacity;    /* number of (L,T) entries allocated */
-  float* lt;              /* [lt_capacity,4] (L.r, L.g, L.b, T) in front of each composited hit */
+  gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit */
   gart_pixel_state* pixel_state; /* [height*width] per-pixel end marker (see gart_pixel_state) */
   /* scratch for sorting and gradient accumulation, size from gart_scratch_bytes */
   void* scratch;
@@ -135,6 +150,8 @@ typedef struct {
   int32_t tiles_x, tiles_y;
   int64_t lt_entries;     /* sum of rectangle areas (Eq. 15 without slack) */
   int64_t pair_count;     /* number of (tile, prim) pairs */
+  double color_step;      /* colour per fixed-point unit of lt and pixel_state (see gart_lt_entry):
+                             a bound on every Gaussian's colour, divided by 2^32 */
   int32_t stage;          /* 0 none, 1 bounds, 2 tile map, 3 forward */
 } gart_frame;
 
@@ -179,9 +196,13 @@ size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, c
  * Culled (rect x0 > x1, area 0): sigma <= alpha_min, ellipsoid behind the
  * camera, no pixel centre covered, non-finite parameters.
  * Then O_prim = exclusive prefix sum of the areas (Sec. 4.3 "primitive
- * offset").  Writes rect, lt_offset, prim_geom, tile_count and frame->n,
- * sh_degree, tiles_x, tiles_y, lt_entries, pair_count, stage.
- * Synchronises `stream` once to copy the two totals to the host:
+ * offset").  Also a bound on the colour of every visible Gaussian in any
+ * direction, 1/2 + sum_l sqrt((2l+1)/(4 pi)) |sh_l| per channel (Cauchy-
+ * Schwarz with the addition theorem of spherical harmonics), which fixes
+ * the frame's colour step = bound / 2^32.  Writes rect, lt_offset,
+ * prim_geom, tile_count and frame->n, sh_degree, tiles_x, tiles_y,
+ * lt_entries, pair_count, color_step, stage.
+ * Synchronises `stream` once to copy the totals to the host:
  * *lt_entries_host = sum A_i (Eq. 15 with lambda_s = 1), *pair_count_host =
  * number of (tile, prim) pairs.  Either host pointer may be NULL.
  * Returns GART_ERR_CAPACITY (after filling the totals) if they exceed
@@ -206,12 +227,13 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
  * hits by (tau, index), composites them front to back and, for every
  * composited hit of Gaussian i at pixel p in tile t, writes
  * lt[idx(i,t,p)] = (L.rgb, T) -- the colour accumulated and the
- * transmittance in front of the hit -- with idx(i,t,p) = O_prim(i) +
+ * transmittance in front of the hit, L in the frame's fixed point -- with idx(i,t,p) = O_prim(i) +
  * O_tile(i,t) + O_pixel(i,t,p) (Eq. 16): tiles of the rectangle in
  * row-major order, pixels row-major inside each tile.  Entries for
  * pixels that are not composited hits are left untouched.
  * image: [height,width,3] float32, written for every pixel.
- * pixel_state is written for every pixel.
+ * pixel_state (end marker, final colour in fixed point, final
+ * transmittance) is written for every pixel.
  * Requires gart_build_tile_map first (else INVALID_ARG). */
 gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
                          gart_frame* frame, float* image, void* stream);
@@ -231,11 +253,12 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
  *     per-Gaussian accumulators with one atomic update per value.
  *   SCATTER: the pixel-centric control (Sec. 3.5): one lane per pixel, one
  *     atomic add per gradient value per composited hit.
- * image must be the forward's output for the same frame; dL_dimage is
+ * The colour in front of and behind each hit comes from the frame's lt and
+ * pixel_state (the forward's image is not read); dL_dimage is
  * [height,width,3] float32.  Requires gart_forward first (else
  * INVALID_ARG). */
 gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
-                          const gart_frame* frame, const float* image, const float* dL_dimage, float* g_means,
+                          const gart_frame* frame, const float* dL_dimage, float* g_means,
                           float* g_log_scales, float* g_quats, float* g_logits, float* g_sh, void* stream);
 
 /* Human-readable name of a status code (static string). */

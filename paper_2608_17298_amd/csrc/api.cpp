@@ -181,12 +181,15 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
 
   f->stage = 0;
   unsigned long long* pair_total = at<unsigned long long>(f->scratch, L.totals);
-  GART_HIP(fill_u32(reinterpret_cast<uint32_t*>(pair_total), 0u, 2, s));
+  uint32_t* color_bound = reinterpret_cast<uint32_t*>(pair_total + 1);
+  GART_HIP(fill_u32(reinterpret_cast<uint32_t*>(pair_total), 0u, 3, s));
   BoundsArgs A{};
   A.means = g->means;
   A.log_scales = g->log_scales;
   A.quats = g->quats;
   A.logits = g->opacity_logits;
+  A.sh = g->sh;
+  A.K = K;
   A.n = n;
   A.cam = make_cam(camera);
   A.alpha_min = settings->alpha_min;
@@ -197,12 +200,18 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   A.tile_count = f->tile_count;
   A.depth_key = at<uint32_t>(f->scratch, L.depth_key);
   A.pair_total = pair_total;
+  A.color_bound = color_bound;
   GART_HIP(launch_bounds(A, s));
   GART_HIP(scan_exclusive_i64(f->lt_offset, f->lt_offset, n, f->lt_offset + n, at<void>(f->scratch, L.scan_tmp), s));
   int64_t host[2] = {0, 0};
   GART_HIP(hipMemcpyAsync(&host[0], f->lt_offset + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GART_HIP(hipMemcpyAsync(&host[1], pair_total, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  uint32_t cb_bits = 0;
+  GART_HIP(hipMemcpyAsync(&cb_bits, color_bound, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
   GART_HIP(hipStreamSynchronize(s));
+  float cb;
+  std::memcpy(&cb, &cb_bits, sizeof cb);
+  f->color_step = double(cb > 0.0f ? cb : 1.0f) / 4294967296.0;
 
   f->n = n;
   f->sh_degree = g->sh_degree;
@@ -302,7 +311,8 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.rect = f->rect;
   A.lt_offset = f->lt_offset;
   A.sh = g->sh;
-  A.lt = reinterpret_cast<float4*>(f->lt);
+  A.lt = reinterpret_cast<uint4*>(f->lt);
+  A.inv_color_step = 1.0 / f->color_step;
   A.image = image;
   A.pixel_state = f->pixel_state;
   A.counters = f->counters;
@@ -314,7 +324,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
 }
 
 gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
-                          const gart_frame* f, const float* image, const float* dL_dimage, float* g_means,
+                          const gart_frame* f, const float* dL_dimage, float* g_means,
                           float* g_log_scales, float* g_quats, float* g_logits, float* g_sh, void* stream) {
   g_err[0] = 0;
   gart_status st;
@@ -324,7 +334,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(f != nullptr, "frame is NULL");
   GART_REQUIRE(f->stage >= 3, "gart_forward must succeed on this frame first");
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
-  GART_REQUIRE(image && dL_dimage, "image/dL_dimage is NULL");
+  GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
   const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode);
@@ -348,8 +358,8 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.pair_offset = f->pair_offset;
   A.tile_count = f->tile_count;
   A.sh = g->sh;
-  A.lt = reinterpret_cast<const float4*>(f->lt);
-  A.image = image;
+  A.lt = reinterpret_cast<const uint4*>(f->lt);
+  A.color_step = float(f->color_step);
   A.dl_dimage = dL_dimage;
   A.pixel_state = f->pixel_state;
   A.acc = at<float>(f->scratch, L.acc);

@@ -3,7 +3,9 @@
 //
 // Per composited hit of Gaussian i at a pixel with upstream gradient g,
 // colour in front L, transmittance in front T (read from the intermediate
-// buffer), final pixel colour C and colour behind S = C - L - T a c:
+// buffer), final pixel colour C and colour behind S = C - L - T a c (C and
+// L are in the frame's fixed point, so C - L is an exact integer difference
+// and S keeps its precision for hits deep behind the front):
 //   dL/dc      = T a g              (zero on a clamped channel)
 //   dL/da      = <g, T c - S / (1 - a)>
 //   dL/dsigma += dL/da rho,   dL/dsh_k += dL/dc Y_k
@@ -33,8 +35,8 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // layout), with explicit fused multiply-adds.
 template <int K>
 __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], double sigma, const float sh[3 * K],
-                                             const float Y[K], const float C[3], const float g[3], float4 lt,
-                                             float acc[acc_width(K)]) {
+                                             const float Y[K], const uint32_t Cq[3], const float g[3], uint4 lt,
+                                             float step, float acc[acc_width(K)]) {
   const float rho = expf(float(-0.5 * D2));
   const float a = float(sigma) * rho;
   float c[3];
@@ -47,15 +49,15 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
     pos[ch] = v > 0.0f;
     c[ch] = pos[ch] ? v : 0.0f;
   }
-  const float T = lt.w;
-  const float Lc[3] = {lt.x, lt.y, lt.z};
+  const float T = __uint_as_float(lt.w);
+  const uint32_t Lq[3] = {lt.x, lt.y, lt.z};
   const float ta = T * a;
   const float inv = 1.0f / (1.0f - a);
   float dlda = 0.0f;
   float dc[3];
 #pragma unroll
   for (int ch = 0; ch < 3; ++ch) {
-    const float S = fmaf(-ta, c[ch], C[ch] - Lc[ch]);  // colour behind the hit
+    const float S = fmaf(-ta, c[ch], __uint2float_rn(Cq[ch] - Lq[ch]) * step);  // colour behind the hit
     dlda = fmaf(g[ch], fmaf(T, c[ch], -S * inv), dlda);
     dc[ch] = pos[ch] ? ta * g[ch] : 0.0f;
   }
@@ -103,7 +105,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   __shared__ double4 s_ray[NT];                 // d.xyz, tau_end
   __shared__ uint32_t s_iend[NT];
   __shared__ __align__(16) float s_Y[NT][KP];
-  __shared__ __align__(16) float s_cg[NT][8];   // C.rgb, g.rgb
+  __shared__ __align__(16) float s_cg[NT][8];   // C.rgb (fixed-point bits), g.rgb
   __shared__ double s_wmax[NT / 64];
   __shared__ uint32_t s_red[NT / 64];
   __shared__ uint32_t s_hist[64];
@@ -127,22 +129,22 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
     double tend = -kInf;
     uint32_t iend = 0;
-    float cg[6] = {0, 0, 0, 0, 0, 0};
+    uint32_t cq[3] = {0, 0, 0};
+    float gg[3] = {0, 0, 0};
     if (valid) {
       const int64_t p = int64_t(py) * A.cam.W + px;
 #pragma unroll
-      for (int ch = 0; ch < 3; ++ch) {
-        cg[ch] = A.image[3 * p + ch];
-        cg[3 + ch] = A.dl_dimage[3 * p + ch];
-      }
+      for (int ch = 0; ch < 3; ++ch) gg[ch] = A.dl_dimage[3 * p + ch];
       const gart_pixel_state st = A.pixel_state[p];
       tend = st.tau_end;
       iend = st.id_end;
+#pragma unroll
+      for (int ch = 0; ch < 3; ++ch) cq[ch] = st.color_fixed[ch];
     }
     s_ray[tid] = make_double4(d[0], d[1], d[2], tend);
     s_iend[tid] = iend;
-    *reinterpret_cast<float4*>(&s_cg[tid][0]) = make_float4(cg[0], cg[1], cg[2], cg[3]);
-    *reinterpret_cast<float4*>(&s_cg[tid][4]) = make_float4(cg[4], cg[5], 0.0f, 0.0f);
+    *reinterpret_cast<uint4*>(&s_cg[tid][0]) = make_uint4(cq[0], cq[1], cq[2], __float_as_uint(gg[0]));
+    *reinterpret_cast<float4*>(&s_cg[tid][4]) = make_float4(gg[1], gg[2], 0.0f, 0.0f);
     double m = tend;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
@@ -249,9 +251,9 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
           return A.lt[base + int64_t(y0 - ya + b / TILE) * w + (b % TILE - (xa - ox))];
         };
         int b = __builtin_ctzll(mask);
-        float4 lt_next = lt_at(b);
+        uint4 lt_next = lt_at(b);
         while (mask) {
-          const float4 lt = lt_next;
+          const uint4 lt = lt_next;
           mask &= mask - 1;
           const int bn = mask ? __builtin_ctzll(mask) : b;
           if (mask) lt_next = lt_at(bn);
@@ -270,11 +272,11 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
             Y[kk + 2] = y4.z;
             Y[kk + 3] = y4.w;
           }
-          const float4 c4 = *reinterpret_cast<const float4*>(&s_cg[lp][0]);
+          const uint4 c4 = *reinterpret_cast<const uint4*>(&s_cg[lp][0]);
           const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
-          const float C[3] = {c4.x, c4.y, c4.z};
-          const float g[3] = {c4.w, g4.x, g4.y};
-          hit_grad_acc<K>(D2, xg, sigma, sh, Y, C, g, lt, acc);
+          const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
+          const float g[3] = {__uint_as_float(c4.w), g4.x, g4.y};
+          hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, g, lt, A.color_step, acc);
           b = bn;
         }
       }
@@ -333,19 +335,19 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
   pixel_ray(A.cam, valid ? px : 0, valid ? py : 0, d);
   float Y[K];
   sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
-  float C[3] = {0, 0, 0}, g[3] = {0, 0, 0};
+  uint32_t Cq[3] = {0, 0, 0};
+  float g[3] = {0, 0, 0};
   double tend = -kInf;
   uint32_t iend = 0;
   if (valid) {
     const int64_t p = int64_t(py) * A.cam.W + px;
 #pragma unroll
-    for (int ch = 0; ch < 3; ++ch) {
-      C[ch] = A.image[3 * p + ch];
-      g[ch] = A.dl_dimage[3 * p + ch];
-    }
+    for (int ch = 0; ch < 3; ++ch) g[ch] = A.dl_dimage[3 * p + ch];
     const gart_pixel_state st = A.pixel_state[p];
     tend = st.tau_end;
     iend = st.id_end;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) Cq[ch] = st.color_fixed[ch];
   }
   bool done = !valid;
   uint32_t n_hits = 0, n_tests = 0, n_atom = 0;
@@ -389,7 +391,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
         if (key_less(tend, iend, tau, id)) continue;
         ++n_hits;
         const int64_t li = __double_as_longlong(row[15]) + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py);
-        const float4 lt = A.lt[li];
+        const uint4 lt = A.lt[li];
         float sh[3 * K];
         const float* shp = A.sh + int64_t(id) * (3 * K);
 #pragma unroll
@@ -397,7 +399,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
         float h[AW];
 #pragma unroll
         for (int v = 0; v < AW; ++v) h[v] = 0.0f;
-        hit_grad_acc<K>(D2, xg, row[13], sh, Y, C, g, lt, h);
+        hit_grad_acc<K>(D2, xg, row[13], sh, Y, Cq, g, lt, A.color_step, h);
         float* dst = A.acc + int64_t(id) * AS;
 #pragma unroll
         for (int v = 0; v < AW; ++v) unsafeAtomicAdd(dst + v, h[v]);

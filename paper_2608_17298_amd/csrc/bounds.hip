@@ -77,6 +77,7 @@ __device__ bool axis_cover(double Qaa, double Qa4, double Q44, int npix, int* lo
 __global__ __launch_bounds__(256) void bounds_kernel(BoundsArgs A) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   uint32_t my_tiles = 0;
+  float my_cb = 0.0f;
   if (i < A.n) {
     const CamParams& c = A.cam;
     float mf[3], lf[3], qf[4];
@@ -201,12 +202,35 @@ __global__ __launch_bounds__(256) void bounds_kernel(BoundsArgs A) {
     A.area[i] = my_tiles ? int64_t(rx1 - rx0 + 1) * int64_t(ry1 - ry0 + 1) : 0;
     A.tile_count[i] = my_tiles;
     A.depth_key[i] = __float_as_uint(key);
+    if (my_tiles) {
+      // Colour bound over all directions: per band l, |sum_m sh_lm Y_lm| <=
+      // |sh_l| sqrt((2l+1)/(4 pi)) (Cauchy-Schwarz and the addition theorem).
+      // Rounded up generously so that the fp32 evaluation of the colour in
+      // the forward stays below it.
+      const float* sp = A.sh + int64_t(3) * A.K * i;
+      double cb = 0.0;
+      for (int ch = 0; ch < 3; ++ch) {
+        double v = 0.5;
+        for (int l = 0; l * l < A.K; ++l) {
+          double ss = 0.0;
+          for (int k = l * l; k < (l + 1) * (l + 1); ++k) ss += double(sp[3 * k + ch]) * double(sp[3 * k + ch]);
+          v += sqrt(ss * double(2 * l + 1) / (4.0 * 3.14159265358979323846));
+        }
+        cb = fmax(cb, v);
+      }
+      my_cb = float(cb * (1.0 + 1.0 / 65536.0));
+      if (!(my_cb >= 0.0f && my_cb < 1e30f)) my_cb = 1e30f;  // non-finite SH: saturate
+    }
   }
-  // block sum of tile counts -> one atomic per wave
+  // block sum of tile counts and max of colour bounds -> one atomic per wave
   unsigned long long t = my_tiles;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) t += __shfl_xor(t, off);
+  for (int off = 32; off > 0; off >>= 1) {
+    t += __shfl_xor(t, off);
+    my_cb = fmaxf(my_cb, __shfl_xor(my_cb, off));
+  }
   if (__lane_id() == 0 && t) atomicAdd(A.pair_total, t);
+  if (__lane_id() == 0 && my_cb > 0.0f) atomicMax(A.color_bound, __float_as_uint(my_cb));
 }
 
 __global__ void gather_counts_kernel(TileMapArgs A) {

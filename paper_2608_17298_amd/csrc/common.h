@@ -128,6 +128,12 @@ __device__ __forceinline__ int xcd_tile(int b, int n) {
 
 __device__ __forceinline__ unsigned lane_id() { return __lane_id(); }
 
+// Non-negative colour -> the frame's fixed point (round to nearest,
+// saturating at 2^32 - 1; the colour bound keeps composited colours below).
+__device__ __forceinline__ uint32_t color_fixed(double v, double inv_step) {
+  return uint32_t(fmin(rint(v * inv_step), 4294967295.0));
+}
+
 // Adds a per-lane count to a device counter with one atomic per wave.  Must
 // be called with the whole wave active.
 __device__ __forceinline__ void count_add(uint64_t* ctr, uint32_t v) {

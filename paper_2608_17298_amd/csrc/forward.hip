@@ -42,7 +42,9 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int kFlushEvery = GART_FWD_FLUSH;
   constexpr double kInf = __builtin_huge_val();
 
+  constexpr int KP = (K + 3) & ~3;  // SH basis row padded to 16 bytes
   __shared__ __align__(16) double s_row[NT * kRow];
+  __shared__ __align__(16) float s_Y[NT][KP];  // SH basis of each pixel's ray
   __shared__ float s_key[NT + 1];
   __shared__ unsigned s_restart;
 
@@ -55,8 +57,12 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
 
   double d[3];
   pixel_ray(A.cam, valid ? px : 0, valid ? py : 0, d);
-  float Y[K];
-  sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
+  {
+    float Y[K];
+    sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
+#pragma unroll
+    for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
+  }
 
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
 
@@ -71,7 +77,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   uint32_t end_id = kNoPrim;
 
   double bt[KB], ba[KB];
-  int64_t bi[KB];
+  uint32_t bi[KB];  // (L,T) offset inside the Gaussian's block
   uint32_t bid[KB], bc[KB];
   int cnt = 0;
   double e_tau = kInf;  // smallest dropped hit (all buffered hits are smaller)
@@ -99,15 +105,22 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     const double a = ba[0];
     const uint32_t id = bid[0];
     const float* shp = A.sh + int64_t(id) * (3 * K);
-    float c[3];
+    const int64_t lt_base = A.lt_offset[id];
+    float c[3] = {0.5f, 0.5f, 0.5f};
 #pragma unroll
-    for (int ch = 0; ch < 3; ++ch) {
-      float v = 0.5f;
+    for (int k = 0; k < KP; k += 4) {
+      const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[tid][k]);
+      const float yk[4] = {y4.x, y4.y, y4.z, y4.w};
 #pragma unroll
-      for (int k = 0; k < K; ++k) v = fmaf(shp[3 * k + ch], Y[k], v);
-      c[ch] = fmaxf(v, 0.0f);
+      for (int u = 0; u < 4; ++u)
+        if (k + u < K)
+#pragma unroll
+          for (int ch = 0; ch < 3; ++ch) c[ch] = fmaf(shp[3 * (k + u) + ch], yk[u], c[ch]);
     }
-    A.lt[bi[0]] = make_float4(float(L0), float(L1), float(L2), float(T));
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) c[ch] = fmaxf(c[ch], 0.0f);
+    A.lt[lt_base + bi[0]] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
+                                       color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
     const double w = T * a;
     L0 = fma(w, double(c[0]), L0);
     L1 = fma(w, double(c[1]), L1);
@@ -189,8 +202,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
                 }
                 if (ins) {
                   const double a = row[13] * exp(-0.5 * D2);
-                  const int64_t li = __double_as_longlong(row[15]) +
-                                     lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py);
+                  const uint32_t li = uint32_t(lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py));
                   int pos = 0;
 #pragma unroll
                   for (int s = 0; s < KB; ++s) pos += (s < cnt && key_less(bt[s], bid[s], tau, id)) ? 1 : 0;
@@ -268,6 +280,10 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     st.tau_end = end_tau;
     st.id_end = end_id;
     st.n_hits = n_hits;
+    st.color_fixed[0] = color_fixed(L0, A.inv_color_step);
+    st.color_fixed[1] = color_fixed(L1, A.inv_color_step);
+    st.color_fixed[2] = color_fixed(L2, A.inv_color_step);
+    st.t_final = float(T);
     A.pixel_state[p] = st;
   }
   if (A.counters) {

@@ -43,6 +43,8 @@ struct BoundsArgs {
   const float* log_scales;
   const float* quats;
   const float* logits;
+  const float* sh;          // [n, K, 3]
+  int32_t K;
   int64_t n;
   CamParams cam;
   double alpha_min;
@@ -53,6 +55,7 @@ struct BoundsArgs {
   uint32_t* tile_count;
   uint32_t* depth_key;      // [n] float bits of the depth lower bound
   unsigned long long* pair_total;  // device accumulator of sum tile_count
+  uint32_t* color_bound;    // float bits, max over visible Gaussians of the colour bound
 };
 hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s);
 
@@ -86,7 +89,8 @@ struct ForwardArgs {
   const int32_t* rect;
   const int64_t* lt_offset;
   const float* sh;
-  float4* lt;
+  uint4* lt;                // (L fixed point, T bits) entries
+  double inv_color_step;    // fixed-point units per unit of colour
   float* image;
   gart_pixel_state* pixel_state;
   uint64_t* counters;
@@ -108,8 +112,8 @@ struct BackwardArgs {
   const int64_t* pair_offset;
   const uint32_t* tile_count;
   const float* sh;
-  const float4* lt;
-  const float* image;
+  const uint4* lt;          // (L fixed point, T bits) entries
+  float color_step;         // colour per fixed-point unit (a power of two times a float)
   const float* dl_dimage;
   const gart_pixel_state* pixel_state;
   // gradient accumulation

@@ -67,7 +67,7 @@ class gart_frame(ctypes.Structure):
                 ("scratch", _P), ("scratch_bytes", ctypes.c_size_t), ("counters", _P),
                 ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
-                ("stage", ctypes.c_int32)]
+                ("color_step", ctypes.c_double), ("stage", ctypes.c_int32)]
 
 
 class GartError(RuntimeError):
@@ -102,7 +102,7 @@ def lib():
         L.gart_forward.restype = ctypes.c_int
         L.gart_forward.argtypes = [_P, _P, _P, _P, _P, _P]
         L.gart_backward.restype = ctypes.c_int
-        L.gart_backward.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.gart_backward.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
         L.gart_status_string.restype = ctypes.c_char_p
         L.gart_status_string.argtypes = [ctypes.c_int]
         L.gart_last_error.restype = ctypes.c_char_p
@@ -219,7 +219,8 @@ class Frame:
         self.tile_count = torch.empty(n1, dtype=torch.int32, **dev)
         self.pair_offset = torch.empty(n1 + 1, dtype=torch.int64, **dev)
         self.tile_range = torch.empty(self.tiles_x * self.tiles_y + 1, dtype=torch.int64, **dev)
-        self.pixel_state = torch.empty((camera.height * camera.width, 2), dtype=torch.int64, **dev)
+        # gart_pixel_state, 32 bytes per pixel
+        self.pixel_state = torch.empty((camera.height * camera.width, 4), dtype=torch.int64, **dev)
         self.counters = torch.zeros(NUM_COUNTERS, dtype=torch.int64, **dev) if counters else None
         self.c = gart_frame()
         self.events = [None] * NUM_EVENTS
@@ -228,7 +229,8 @@ class Frame:
         self._alloc_pairs(pair_capacity)
 
     def _alloc_lt(self, cap):
-        self.lt = torch.empty((max(int(cap), 1), 4), dtype=torch.float32, device=self.device)
+        # gart_lt_entry: three fixed-point colour words and the float bits of T
+        self.lt = torch.empty((max(int(cap), 1), 4), dtype=torch.int32, device=self.device)
         self.lt_capacity = int(cap)
 
     def _alloc_pairs(self, cap):
@@ -276,6 +278,24 @@ class Frame:
         return int(self.c.lt_entries)
 
     @property
+    def color_step(self) -> float:
+        """Colour per fixed-point unit of the (L,T) entries and pixel colours."""
+        return float(self.c.color_step)
+
+    def lt_entries_host(self, index: torch.Tensor):
+        """(L [m,3] float64, T [m] float32) of the listed (L,T) entries, on the host."""
+        raw = self.lt[index].cpu().numpy()
+        L = raw[:, :3].view(np.uint32).astype(np.float64) * self.color_step
+        return L, raw[:, 3].copy().view(np.float32)
+
+    def pixel_state_host(self) -> dict:
+        """gart_pixel_state fields of every pixel, on the host."""
+        ps = self.pixel_state.cpu().numpy()
+        w = ps.view(np.uint32)
+        return dict(tau_end=ps[:, 0].copy().view(np.float64), id_end=w[:, 2].copy(), n_hits=w[:, 3].copy(),
+                    color=w[:, 4:7].astype(np.float64) * self.color_step, t_final=w[:, 7].copy().view(np.float32))
+
+    @property
     def pair_count(self):
         return int(self.c.pair_count)
 
@@ -316,17 +336,16 @@ def gart_forward(g: Gaussians, camera: gart_camera, settings: gart_settings, fra
                               _ptr(image), _stream(stream)), "gart_forward")
 
 
-def gart_backward(g: Gaussians, camera: gart_camera, settings: gart_settings, frame: Frame, image: torch.Tensor,
+def gart_backward(g: Gaussians, camera: gart_camera, settings: gart_settings, frame: Frame,
                   dl_dimage: torch.Tensor, grads: dict, stream=None):
     """Backward (Sec. 4.4); grads holds float32 device tensors means, log_scales,
     quats, logits, sh shaped like the parameters (overwritten)."""
-    for t in (image, dl_dimage):
-        if t.dtype != torch.float32 or t.shape != (camera.height, camera.width, 3):
-            raise ValueError("image and dl_dimage must be float32 [H,W,3]")
+    if dl_dimage.dtype != torch.float32 or dl_dimage.shape != (camera.height, camera.width, 3):
+        raise ValueError("dl_dimage must be float32 [H,W,3]")
     gs = g.c_struct()
     fs = frame.c_struct()
     _check(lib().gart_backward(ctypes.byref(gs), ctypes.byref(camera), ctypes.byref(settings), ctypes.byref(fs),
-                               _ptr(image), _ptr(dl_dimage), _ptr(grads["means"]), _ptr(grads["log_scales"]),
+                               _ptr(dl_dimage), _ptr(grads["means"]), _ptr(grads["log_scales"]),
                                _ptr(grads["quats"]), _ptr(grads["logits"]), _ptr(grads["sh"]),
                                _stream(stream)), "gart_backward")
 

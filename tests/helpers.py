@@ -73,20 +73,20 @@ def run_gpu(scene, mode="gather", tile=None, dl=None, counters=True, keep_frame=
     gart.gart_forward(g, cam, st, frame, image)
     dlt = torch.from_numpy(np.ascontiguousarray(scene.dl_dimage if dl is None else dl, dtype=np.float32)).cuda()
     grads = gart.empty_grads(g)
-    gart.gart_backward(g, cam, st, frame, image, dlt, grads)
+    gart.gart_backward(g, cam, st, frame, dlt, grads)
     torch.cuda.synchronize()
     n = scene.n
     P = frame.pair_count
-    ps = frame.pixel_state.cpu().numpy()
+    ps = frame.pixel_state_host()
     out = dict(
         rect=frame.rect.cpu().numpy()[:n], lt_offset=frame.lt_offset.cpu().numpy()[:n + 1],
         tile_count=frame.tile_count.cpu().numpy()[:n].view(np.uint32), geom=frame.prim_geom.cpu().numpy()[:n],
         pair_tile=frame.pair_tile.cpu().numpy()[:P].view(np.uint32),
         pair_prim=frame.pair_prim.cpu().numpy()[:P].view(np.uint32),
         pair_offset=frame.pair_offset.cpu().numpy()[:n + 1], tile_range=frame.tile_range.cpu().numpy(),
-        image=image.cpu().numpy(), tau_end=ps[:, 0].copy().view(np.float64),
-        id_end=(ps[:, 1] & 0xffffffff).astype(np.int64),
-        n_hits=(ps[:, 1] >> 32).astype(np.int64), lt_entries=frame.lt_entries, pair_count=P,
+        image=image.cpu().numpy(), tau_end=ps["tau_end"], id_end=ps["id_end"].astype(np.int64),
+        n_hits=ps["n_hits"].astype(np.int64), state_color=ps["color"], t_final=ps["t_final"],
+        color_step=frame.color_step, lt_entries=frame.lt_entries, pair_count=P,
         grads={k: v.cpu().numpy().astype(np.float64) for k, v in grads.items()},
         counters=None if frame.counters is None else frame.counters.cpu().numpy())
     if keep_frame:

@@ -1,0 +1,85 @@
+"""GPU parity at the full workload sizes, in the launch configuration that
+bench.py times (8x8 tiles, gather backward), on outputs the oracle computes
+one by one: every rectangle, a sample of tiles' Gaussian sets, a sample of
+pixels, and the complete gradients of a sample of Gaussians (the oracle
+renders every pixel of those Gaussians' rectangles, so their gradients are
+exact).
+
+The upstream gradient is the generator's +-1 field (the distribution of an
+L1 loss gradient); rendering the perturbed-means target at these sizes on
+the CPU would take the oracle minutes.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import rel_l2, run_gpu
+from paper_2608_17298_amd.scenes import make_scene
+
+pytestmark = pytest.mark.gpu
+
+PIX_TOL = 1e-5
+GRAD_TOL = 1e-4
+AMBIG = 1e-9
+GROUPS = ["means", "log_scales", "quats", "logits", "sh"]
+
+
+def _brute_tile(rect, state, t, W, H, ts):
+    ntx = -(-W // ts)
+    tx, ty = t % ntx, t // ntx
+    x0, x1, y0, y1 = tx * ts, min(W - 1, tx * ts + ts - 1), ty * ts, min(H - 1, ty * ts + ts - 1)
+    hit = (state == 0) & (rect[:, 0] <= x1) & (rect[:, 2] >= x0) & (rect[:, 1] <= y1) & (rect[:, 3] >= y0)
+    return np.nonzero(hit)[0]
+
+
+@pytest.mark.parametrize("name,max_area", [("1m", 2500), ("4m", 2500), ("stress", 2500)])
+def test_fullsize_sampled(name, max_area):
+    rng = np.random.default_rng(2608)
+    sc = make_scene(name)
+    print(f"[{name}] N={sc.n} {sc.camera.width}x{sc.camera.height}", flush=True)
+    gpu = run_gpu(sc, mode="gather")
+    o = oracle.OracleScene(sc)
+    info = o.prim_info()
+    W, H, ts = o.W, o.H, sc.tile
+
+    # Rectangles and primitive offsets, every Gaussian.
+    assert np.array_equal(gpu["rect"], info.rect)
+    assert np.array_equal(np.diff(gpu["lt_offset"]), info.area)
+
+    # Gaussian set of sampled tiles.
+    n_tiles = len(gpu["tile_range"]) - 1
+    tr = gpu["tile_range"]
+    for t in rng.choice(n_tiles, 150, replace=False):
+        got = np.sort(gpu["pair_prim"][tr[t]:tr[t + 1]].astype(np.int64))
+        assert np.array_equal(got, _brute_tile(info.rect, info.state, t, W, H, ts)), t
+
+    # Sampled pixels: colour, composited count and end marker.
+    pix = np.sort(rng.choice(W * H, 3000, replace=False))
+    ren = o.render(pix)
+    ok = ren["margin"] >= AMBIG
+    img = gpu["image"].reshape(-1, 3)[pix]
+    assert np.abs(img - ren["color"])[ok].max() <= PIX_TOL
+    assert np.array_equal(gpu["n_hits"][pix][ok], ren["n_included"][ok])
+    term = ok & np.isfinite(ren["tau_end"])
+    assert np.array_equal(gpu["id_end"][pix][term], ren["id_end"][term])
+
+    # Complete gradients of sampled Gaussians with modest rectangles, drawn
+    # from those the oracle composites at one of the sampled pixels (in a
+    # deep scene most Gaussians are hidden and have zero gradient).
+    _, prim, _, _ = o.records(pix, ren["n_included"])
+    vis = np.unique(prim)
+    cand = vis[(info.area[vis] >= 30) & (info.area[vis] <= max_area)]
+    assert len(cand) >= 24
+    sel = np.sort(rng.choice(cand, 24, replace=False))
+    pixels = []
+    for i in sel:
+        x0, y0, x1, y1 = info.rect[i]
+        ys, xs = np.mgrid[y0:y1 + 1, x0:x1 + 1]
+        pixels.append((ys * W + xs).ravel())
+    pixels = np.unique(np.concatenate(pixels))
+    print(f"[{name}] oracle backward over {len(pixels)} pixels", flush=True)
+    ref = o.backward(sc.dl_dimage, pixels=pixels)
+    assert (np.abs(ref["means"][sel]).sum(axis=1) > 0).all()
+    for k in GROUPS:
+        e = rel_l2(gpu["grads"][k][sel], ref[k][sel])
+        assert e <= GRAD_TOL, (k, e)

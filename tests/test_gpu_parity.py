@@ -105,6 +105,12 @@ def test_forward_pixels_and_markers(name):
     term = np.isfinite(ren["tau_end"]) & ok
     assert np.array_equal(gpu["id_end"][term], ren["id_end"][term])
     assert np.all(~np.isfinite(gpu["tau_end"][~np.isfinite(ren["tau_end"]) & ok]))
+    # final colour in the frame's fixed point (half a step of rounding) and
+    # final transmittance, as the backward reads them
+    assert np.abs(gpu["state_color"] - ren["color"])[ok].max() <= PIX_TOL
+    slack = 0.5 * gpu["color_step"] + 1.2e-7 * np.maximum(1.0, np.abs(img))
+    assert np.all(np.abs(gpu["state_color"] - img.astype(np.float64)) <= slack)
+    assert np.abs(gpu["t_final"].astype(np.float64) - ren["T_final"])[ok].max() <= 1e-6
 
 
 @pytest.mark.parametrize("name", ["tiny", "small_reduced", "random_sh3"])
@@ -119,9 +125,9 @@ def test_forward_lt_entries(name):
     owner = np.repeat(pix, np.diff(off))
     idx = o.lt_index(sc.tile, prim, owner)
     assert (idx >= 0).all()
-    lt = gpu["frame"].lt[torch.from_numpy(idx).cuda()].cpu().numpy().astype(np.float64)
-    assert np.abs(lt[:, :3] - LT[:, :3]).max() <= PIX_TOL
-    assert np.abs(lt[:, 3] - LT[:, 3]).max() <= 1e-6
+    L, T = gpu["frame"].lt_entries_host(torch.from_numpy(idx).cuda())
+    assert np.abs(L - LT[:, :3]).max() <= PIX_TOL
+    assert np.abs(T.astype(np.float64) - LT[:, 3]).max() <= 1e-6
 
 
 @pytest.mark.parametrize("mode", ["gather", "gather_atomic", "scatter"])
@@ -235,7 +241,7 @@ def test_invalid_args_on_device_path():
     f = gart.prepare(g, cam, st)
     img = torch.empty((cam.height, cam.width, 3), device="cuda")
     with pytest.raises(gart.GartError):  # backward before forward
-        gart.gart_backward(g, cam, st, f, img, img, gart.empty_grads(g))
+        gart.gart_backward(g, cam, st, f, img, gart.empty_grads(g))
     bad = gart.make_settings(16)
     bad.t_min = 0.0
     with pytest.raises(gart.GartError):
