@@ -43,7 +43,7 @@ struct Layout {
       acc, rows, row_flag, total;
 };
 
-Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode) {
+Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
   Layout L{};
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -64,8 +64,9 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode) {
   L.totals = take(64);
   const size_t AS = size_t(acc_stride(K));
   L.acc = take(mode == GART_BACKWARD_GATHER ? 4 : size_t(nn) * AS * 4);
-  L.rows = take(mode == GART_BACKWARD_GATHER ? size_t(pc) * AS * 4 : 4);
-  L.row_flag = take(mode == GART_BACKWARD_GATHER ? size_t(pc) : 4);
+  const size_t rpp = size_t(tile) * size_t(tile) / 64;  // partial rows per pair (64-pixel groups)
+  L.rows = take(mode == GART_BACKWARD_GATHER ? size_t(pc) * rpp * AS * 4 : 4);
+  L.row_flag = take(mode == GART_BACKWARD_GATHER ? size_t(pc) * rpp : 4);
   L.total = off;
   return L;
 }
@@ -158,7 +159,8 @@ size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, c
   (void)camera;
   const int deg = std::min(std::max(sh_degree, 0), 3);
   const int mode = settings ? settings->backward_mode : GART_BACKWARD_GATHER;
-  return make_layout(std::max<int64_t>(n, 0), (deg + 1) * (deg + 1), std::max<int64_t>(pair_capacity, 0), mode)
+  return make_layout(std::max<int64_t>(n, 0), (deg + 1) * (deg + 1), std::max<int64_t>(pair_capacity, 0), mode,
+                     settings && settings->tile == 16 ? 16 : 8)
       .total;
 }
 
@@ -175,7 +177,7 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   GART_REQUIRE(f->lt_offset != nullptr && f->scratch != nullptr, "frame lt_offset/scratch is NULL");
   if (n > 0) GART_REQUIRE(f->rect && f->prim_geom && f->tile_count, "frame per-Gaussian buffer is NULL");
   GART_REQUIRE(f->rect == nullptr || aligned16(f->rect), "rect must be 16-byte aligned");
-  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode);
+  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
@@ -246,7 +248,7 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   GART_REQUIRE(P <= f->pair_capacity, "pair capacity");
   if (P > 0) GART_REQUIRE(f->pair_tile && f->pair_prim, "frame pair buffers are NULL");
   const int K = (f->sh_degree + 1) * (f->sh_degree + 1);
-  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode);
+  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
@@ -337,7 +339,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
-  const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode);
+  const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode, settings->tile);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu (backward mode %d)", f->scratch_bytes,
                L.total, settings->backward_mode);
   GART_REQUIRE(aligned16(f->scratch), "scratch must be 16-byte aligned");

@@ -81,43 +81,95 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
 }
 
 // ---------------------------------------------------------------------------
-// Gather: one workgroup per tile; each lane owns whole (tile, Gaussian)
-// pairs.  Per-pixel state (ray direction, end marker, SH basis, colour and
-// upstream gradient) is staged in LDS once per tile, pixel-major so a lane
-// reads one pixel's fields with 128-bit loads.  Only pairs whose depth bound
-// lies in front of the tile's last ray end are visited (a prefix of the
-// depth-ordered list).  Visited pairs are dealt to lanes largest first
-// (counting sort by pixel count in LDS) so that lanes working in the same
-// round have similar loads.  Each pair first tests its pixels into a
-// bit mask of composited hits, then accumulates the gradient of those hits
-// in registers, and finally writes one partial row (or adds it atomically).
+// Gather: one workgroup per tile.  The tile's pixels form G = TILE^2 / 64
+// groups of 64 pixels (whole rows, one wave each); the unit of work is a
+// (pair, group): the pixels of one group that one Gaussian's rectangle
+// covers.  Per tile:
+//  1. Per-pixel state (ray direction, end marker, SH basis, colour and
+//     upstream gradient) is staged in LDS.  Each group's pixels are ranked
+//     by their ray end, so that "the pixels whose ray ends at or behind
+//     depth k" is one of 65 prefix masks, found by a binary search.
+//  2. Only pairs whose depth bound lies in front of the tile's last ray end
+//     are visited (a prefix of the depth-ordered list), in LDS passes of up
+//     to kUnits units.
+//  3. Candidates, without a ray test: the unit's rectangle rows and columns
+//     AND the pixels whose ray ends at or behind the pair's depth bound.
+//  4. Phase 1: each lane tests the candidate pixels of one unit and keeps
+//     the mask of composited hits.  Units are dealt in order of candidate
+//     count, so the lanes of a round run loops of equal length.
+//  5. Phase 2: each lane accumulates the gradient of one unit's composited
+//     hits in registers (units dealt in order of hit count) and writes one
+//     partial row (or adds it atomically).
 // ---------------------------------------------------------------------------
-constexpr int kSortChunk = 2048;  // visited pairs ordered per LDS pass
+constexpr int kUnits = 512;  // units per LDS pass
+
+// Deals the units of a pass by bucket (0 first; 0xff = dropped): counting
+// sort into s_order.  s_hist holds the bucket counts on entry and is zero on
+// return.  Returns the number of units kept.  Called by the whole block.
+template <int NT>
+__device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint32_t* s_hist, uint16_t* s_order,
+                                          uint32_t* s_total) {
+  __syncthreads();  // buckets and counts complete
+  if (threadIdx.x < 64) {
+    const uint32_t c = s_hist[threadIdx.x];
+    uint32_t inc = c;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t u = __shfl_up(inc, off);
+      if (__lane_id() >= unsigned(off)) inc += u;
+    }
+    s_hist[threadIdx.x] = inc - c;
+    if (threadIdx.x == 63) *s_total = inc;
+  }
+  __syncthreads();
+  for (int u = threadIdx.x; u < nu; u += NT) {
+    const uint8_t b = s_bucket[u];
+    if (b != 0xff) s_order[atomicAdd(&s_hist[b], 1u)] = uint16_t(u);
+  }
+  __syncthreads();
+  const int kept = int(*s_total);
+  if (threadIdx.x < 64) s_hist[threadIdx.x] = 0;
+  __syncthreads();
+  return kept;
+}
 
 template <int TILE, int K, bool ATOMIC>
 __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   constexpr int NT = TILE * TILE;
-  constexpr int kChunkRows = 64 / TILE;  // rows of a tile whose pixels fit one 64-bit mask
+  constexpr int G = NT / 64;      // pixel groups (waves) per tile
+  constexpr int R = 64 / TILE;    // tile rows per group
+  constexpr int kPairs = kUnits / G;
   constexpr int AW = acc_width(K), AS = acc_stride(K);
-  constexpr int KP = (K + 3) & ~3;       // SH basis row padded to 16 bytes
+  constexpr int KP = (K + 3) & ~3;  // SH basis row padded to 16 bytes
   constexpr double kInf = __builtin_huge_val();
+  // one bit per row start of a group: rows r = 0..R-1 at bit r * TILE
+  constexpr uint64_t kRowOnes = TILE == 8 ? 0x0101010101010101ull : 0x0001000100010001ull;
+  static_assert(NT % 64 == 0 && (TILE == 8 || TILE == 16), "tile of 8 or 16");
 
   __shared__ double4 s_ray[NT];                 // d.xyz, tau_end
   __shared__ uint32_t s_iend[NT];
   __shared__ __align__(16) float s_Y[NT][KP];
   __shared__ __align__(16) float s_cg[NT][8];   // C.rgb (fixed-point bits), g.rgb
-  __shared__ double s_wmax[NT / 64];
-  __shared__ uint32_t s_red[NT / 64];
+  __shared__ double s_tsort[G][64];             // ray ends of a group, descending
+  __shared__ uint32_t s_pix[G][64];             // pixel of each rank
+  __shared__ uint64_t s_prefix[G][65];          // pixels of the k latest ray ends
+  __shared__ double s_wmax[G];
+  __shared__ uint32_t s_red[G];
   __shared__ uint32_t s_hist[64];
-  __shared__ uint8_t s_bucket[kSortChunk];
-  __shared__ uint16_t s_order[kSortChunk];
+  __shared__ uint32_t s_total;
+  __shared__ uint64_t s_mask[kUnits];
+  __shared__ uint32_t s_id[kPairs];
+  __shared__ uint8_t s_bucket[kUnits];
+  __shared__ uint16_t s_order[kUnits];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
   const int tile = xcd_tile(blockIdx.x, n_tiles);
   const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
   const int ox = tx * TILE, oy = ty * TILE;
   const int tid = threadIdx.x;
+  const int wv = tid / 64, lane = tid % 64;
 
+  double my_tend;
   {
     const int px = ox + tid % TILE, py = oy + tid / TILE;
     const bool valid = px < A.cam.W && py < A.cam.H;
@@ -127,7 +179,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
 #pragma unroll
     for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
-    double tend = -kInf;
+    double tend = -kInf;  // a pixel outside the image is never a candidate
     uint32_t iend = 0;
     uint32_t cq[3] = {0, 0, 0};
     float gg[3] = {0, 0, 0};
@@ -148,12 +200,36 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     double m = tend;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
-    if (__lane_id() == 0) s_wmax[tid / 64] = m;
+    if (lane == 0) s_wmax[wv] = m;
+    my_tend = tend;
   }
   __syncthreads();
+  {
+    // Rank of this pixel's ray end within its group (latest first, ties by
+    // pixel), then prefix masks by rank.
+    int rank = 0;
+    for (int q = 0; q < 64; ++q) {
+      const double t = s_ray[wv * 64 + q].w;
+      rank += (t > my_tend || (t == my_tend && q < lane)) ? 1 : 0;
+    }
+    s_tsort[wv][rank] = my_tend;
+    s_pix[wv][rank] = uint32_t(lane);
+  }
+  __syncthreads();
+  {
+    uint64_t pm = 1ull << s_pix[wv][lane];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint64_t u = __shfl_up(pm, off);
+      if (lane >= off) pm |= u;
+    }
+    s_prefix[wv][lane + 1] = pm;
+    if (lane == 0) s_prefix[wv][0] = 0;
+    if (tid < 64) s_hist[tid] = 0;
+  }
   double tmax = s_wmax[0];
 #pragma unroll
-  for (int w = 1; w < NT / 64; ++w) tmax = fmax(tmax, s_wmax[w]);
+  for (int w = 1; w < G; ++w) tmax = fmax(tmax, s_wmax[w]);
 
   // Number of visited pairs: the list is ordered by depth bound, so they
   // form its prefix of pairs whose bound is <= tmax.
@@ -165,122 +241,137 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) nv += __shfl_xor(nv, off);
-  if (__lane_id() == 0) s_red[tid / 64] = nv;
+  if (lane == 0) s_red[wv] = nv;
   __syncthreads();
   int64_t V = 0;
 #pragma unroll
-  for (int w = 0; w < NT / 64; ++w) V += s_red[w];
+  for (int w = 0; w < G; ++w) V += s_red[w];
 
   uint32_t n_pairs = 0, n_hits = 0, n_tests = 0, n_atom = 0, n_active = 0;
-  for (int64_t c0 = 0; c0 < V; c0 += kSortChunk) {
-    const int nc = int(min<int64_t>(kSortChunk, V - c0));
-    __syncthreads();  // the previous chunk's order is no longer read
-    if (tid < 64) s_hist[tid] = 0;
-    __syncthreads();
+  for (int64_t c0 = 0; c0 < V; c0 += kPairs) {
+    const int nc = int(min<int64_t>(kPairs, V - c0));
+    const int nu = nc * G;
+    // Candidates of every unit of the pass.
     for (int q = tid; q < nc; q += NT) {
-      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(A.pair_prim[beg + c0 + q]));
-      const int npx = (min(r.z, ox + TILE - 1) - max(r.x, ox) + 1) * (min(r.w, oy + TILE - 1) - max(r.y, oy) + 1);
-      const int bk = 63 - min(63, (npx - 1) * 64 / NT);  // larger footprints first
-      s_bucket[q] = uint8_t(bk);
-      atomicAdd(&s_hist[bk], 1u);
-    }
-    __syncthreads();
-    if (tid < 64) {  // exclusive scan of the 64 bucket counts (one wave)
-      const uint32_t c = s_hist[tid];
-      uint32_t inc = c;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t u = __shfl_up(inc, off);
-        if (__lane_id() >= unsigned(off)) inc += u;
-      }
-      s_hist[tid] = inc - c;
-    }
-    __syncthreads();
-    for (int q = tid; q < nc; q += NT) s_order[atomicAdd(&s_hist[s_bucket[q]], 1u)] = uint16_t(q);
-    __syncthreads();
-
-    for (int q = tid; q < nc; q += NT) {
-      const int64_t j = beg + c0 + s_order[q];
-      const uint32_t i = A.pair_prim[j];
-      const double* G = A.geom + int64_t(kGeomStride) * i;
+      const uint32_t i = A.pair_prim[beg + c0 + q];
+      s_id[q] = i;
       ++n_pairs;
+      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
+      const double key = A.geom[int64_t(kGeomStride) * i + kGeoKey];
+      const int xa = max(r.x, ox), xb = min(r.z, ox + TILE - 1);
+      const uint64_t cols = ((1ull << (xb - xa + 1)) - 1ull) << (xa - ox);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int gy0 = oy + g * R;
+        const int ya = max(r.y, gy0), yb = min(r.w, gy0 + R - 1);
+        uint64_t m = 0;
+        if (ya <= yb) {
+          const uint64_t rows = (kRowOnes >> ((R - 1 - (yb - ya)) * TILE)) << ((ya - gy0) * TILE);
+          int lo = 0, hi = 64;  // number of pixels whose ray ends at or behind key
+          while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (s_tsort[g][mid] >= key)
+              lo = mid + 1;
+            else
+              hi = mid;
+          }
+          m = cols * rows & s_prefix[g][lo];
+        }
+        const int u = q * G + g;
+        s_mask[u] = m;
+        const int c = __popcll(m);
+        s_bucket[u] = c ? uint8_t(64 - c) : uint8_t(0xff);
+        if (c) atomicAdd(&s_hist[64 - c], 1u);
+      }
+    }
+    const int nu1 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total);
+
+    // Phase 1: ray tests of the candidates -> mask of composited hits.
+    for (int o = tid; o < nu1; o += NT) {
+      const int u = s_order[o], g = u % G;
+      const uint32_t i = s_id[u / G];
+      const double* Gm = A.geom + int64_t(kGeomStride) * i;
       double W[9], og[3];
 #pragma unroll
-      for (int k = 0; k < 9; ++k) W[k] = G[k];
+      for (int k = 0; k < 9; ++k) W[k] = Gm[k];
 #pragma unroll
-      for (int k = 0; k < 3; ++k) og[k] = G[kGeoOg + k];
-      const double D2c = G[kGeoD2c], sigma = G[kGeoSigma], key = G[kGeoKey];
+      for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
+      const double D2c = Gm[kGeoD2c];
+      uint64_t m = s_mask[u], hit = 0;
+      while (m) {
+        const int b = __builtin_ctzll(m);
+        m &= m - 1;
+        const int lp = g * 64 + b;
+        const double4 ry = s_ray[lp];
+        const double d[3] = {ry.x, ry.y, ry.z};
+        double tau, D2, xg[3];
+        ++n_tests;
+        if (ray_hit(W, og, D2c, d, &tau, &D2, xg) && !key_less(ry.w, s_iend[lp], tau, i)) hit |= 1ull << b;
+      }
+      s_mask[u] = hit;
+      const int c = __popcll(hit);
+      s_bucket[u] = c ? uint8_t(64 - c) : uint8_t(0xff);
+      if (c) atomicAdd(&s_hist[64 - c], 1u);
+    }
+    const int nu2 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total);
+
+    // Phase 2: gradient of each unit's composited hits, in row-major order.
+    for (int o = tid; o < nu2; o += NT) {
+      const int u = s_order[o], g = u % G;
+      const uint32_t i = s_id[u / G];
+      const double* Gm = A.geom + int64_t(kGeomStride) * i;
+      double W[9], og[3];
+#pragma unroll
+      for (int k = 0; k < 9; ++k) W[k] = Gm[k];
+#pragma unroll
+      for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
+      const double D2c = Gm[kGeoD2c], sigma = Gm[kGeoSigma];
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
       float sh[3 * K];
       const float* shp = A.sh + int64_t(i) * (3 * K);
 #pragma unroll
       for (int k = 0; k < 3 * K; ++k) sh[k] = shp[k];
       const int xa = max(r.x, ox), xb = min(r.z, ox + TILE - 1);
-      const int ya = max(r.y, oy), yb = min(r.w, oy + TILE - 1);
-      const int64_t base = A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, xa, ya);
+      const int ya = max(r.y, oy);
       const int w = xb - xa + 1;
+      // (L,T) index of pixel b of the group: O_prim + O_tile + row-major
+      // offset inside rect cap tile (Eq. 16).
+      const int64_t base = A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, xa, ya) +
+                           int64_t(oy + g * R - ya) * w + (ox - xa);
+      auto lt_at = [&](int b) { return A.lt[base + int64_t(b / TILE) * w + (b % TILE)]; };
       float acc[AW];
 #pragma unroll
       for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
-      bool any = false;
-      // Rows of rect cap tile in chunks of at most 64 pixels.
-      for (int y0 = ya; y0 <= yb; y0 += kChunkRows) {
-        const int y1 = min(yb, y0 + kChunkRows - 1);
-        const int lp0 = (y0 - oy) * TILE;
-        // Phase 1: which pixels hold a composited hit of this Gaussian (bit =
-        // pixel index within the chunk).  A pixel whose ray ended in front of
-        // the Gaussian's depth bound is skipped without a test.
-        uint64_t mask = 0;
-        for (int y = y0; y <= y1; ++y) {
-          for (int x = xa; x <= xb; ++x) {
-            const int b = (y - y0) * TILE + (x - ox);
-            const double4 ry = s_ray[lp0 + b];
-            if (key > ry.w) continue;
-            const double d[3] = {ry.x, ry.y, ry.z};
-            double tau, D2, xg[3];
-            ++n_tests;
-            if (ray_hit(W, og, D2c, d, &tau, &D2, xg) && !key_less(ry.w, s_iend[lp0 + b], tau, i))
-              mask |= 1ull << b;
-          }
-        }
-        if (!mask) continue;
-        any = true;
-        // Phase 2: the gradient of each composited hit, in row-major order.
-        // (L,T) index: base + row offset within rect cap tile + column offset.
-        auto lt_at = [&](int b) {
-          return A.lt[base + int64_t(y0 - ya + b / TILE) * w + (b % TILE - (xa - ox))];
-        };
-        int b = __builtin_ctzll(mask);
-        uint4 lt_next = lt_at(b);
-        while (mask) {
-          const uint4 lt = lt_next;
-          mask &= mask - 1;
-          const int bn = mask ? __builtin_ctzll(mask) : b;
-          if (mask) lt_next = lt_at(bn);
-          const int lp = lp0 + b;
-          const double4 ry = s_ray[lp];
-          const double d[3] = {ry.x, ry.y, ry.z};
-          double tau, D2, xg[3];
-          ray_hit(W, og, D2c, d, &tau, &D2, xg);
-          ++n_hits;
-          float Y[KP];
+      uint64_t m = s_mask[u];
+      int b = __builtin_ctzll(m);
+      uint4 lt_next = lt_at(b);
+      while (m) {
+        const uint4 lt = lt_next;
+        m &= m - 1;
+        const int bn = m ? __builtin_ctzll(m) : b;
+        if (m) lt_next = lt_at(bn);
+        const int lp = g * 64 + b;
+        const double4 ry = s_ray[lp];
+        const double d[3] = {ry.x, ry.y, ry.z};
+        double tau, D2, xg[3];
+        ray_hit(W, og, D2c, d, &tau, &D2, xg);
+        ++n_hits;
+        float Y[KP];
 #pragma unroll
-          for (int kk = 0; kk < KP; kk += 4) {
-            const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[lp][kk]);
-            Y[kk] = y4.x;
-            Y[kk + 1] = y4.y;
-            Y[kk + 2] = y4.z;
-            Y[kk + 3] = y4.w;
-          }
-          const uint4 c4 = *reinterpret_cast<const uint4*>(&s_cg[lp][0]);
-          const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
-          const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
-          const float g[3] = {__uint_as_float(c4.w), g4.x, g4.y};
-          hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, g, lt, A.color_step, acc);
-          b = bn;
+        for (int kk = 0; kk < KP; kk += 4) {
+          const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[lp][kk]);
+          Y[kk] = y4.x;
+          Y[kk + 1] = y4.y;
+          Y[kk + 2] = y4.z;
+          Y[kk + 3] = y4.w;
         }
+        const uint4 c4 = *reinterpret_cast<const uint4*>(&s_cg[lp][0]);
+        const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
+        const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
+        const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
+        hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, gr, lt, A.color_step, acc);
+        b = bn;
       }
-      if (!any) continue;
       ++n_active;
       if constexpr (ATOMIC) {
         float* dst = A.acc + int64_t(i) * AS;
@@ -289,7 +380,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
         n_atom += AW;
       } else {
         const int tx0 = r.x / TILE, ty0 = r.y / TILE, tx1 = r.z / TILE;
-        const int64_t row = A.pair_offset[i] + int64_t(ty - ty0) * (tx1 - tx0 + 1) + (tx - tx0);
+        const int64_t row = (A.pair_offset[i] + int64_t(ty - ty0) * (tx1 - tx0 + 1) + (tx - tx0)) * G + g;
         float4* dst = reinterpret_cast<float4*>(A.rows + row * AS);
 #pragma unroll
         for (int v = 0; v < AS; v += 4) {
@@ -303,6 +394,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
         A.row_flag[row] = 1;
       }
     }
+    __syncthreads();  // the pass's LDS arrays are rewritten by the next pass
   }
   if (A.counters) {
     count_add(A.counters + GART_CNT_BWD_PAIRS, n_pairs);
@@ -419,7 +511,8 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 // Per-Gaussian reduction of the pair rows (gather mode) or read of the
 // atomic accumulators, then the chain rule to the raw parameters.  A block
 // serves 64 Gaussians.  Reduction: sixteen lanes per Gaussian, lane q reads
-// float4 q of each active row (rows are contiguous in emission order), 16
+// float4 q of each active row (a Gaussian's rows are contiguous: its pairs in
+// emission order, rows_per_pair pixel groups each), 16
 // row flags are read at once and up to four rows are loaded per step.
 // Chain rule: one Gaussian per lane of the first wave.  SH gradients: all
 // threads, coalesced.
@@ -445,7 +538,7 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
     float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if constexpr (ROWS) {
       const float4* rows = reinterpret_cast<const float4*>(A.rows);
-      const int64_t r0 = live ? A.pair_offset[i] : 0, r1 = r0 + tc;
+      const int64_t r0 = live ? A.pair_offset[i] * A.rows_per_pair : 0, r1 = r0 + int64_t(tc) * A.rows_per_pair;
       for (int64_t rb = r0; rb < r1; rb += kReduceLanes) {
         const int64_t rq = rb + q;
         const bool act = rq < r1 && A.row_flag[rq] != 0;
@@ -540,12 +633,14 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
 }
 
 template <int TILE, int K>
-hipError_t launch_tk(const BackwardArgs& a, hipStream_t s) {
+hipError_t launch_tk(const BackwardArgs& args, hipStream_t s) {
   constexpr int AS = acc_stride(K);
+  BackwardArgs a = args;
+  a.rows_per_pair = TILE * TILE / 64;
   const int n_tiles = a.tiles_x * a.tiles_y;
   hipError_t e = hipSuccess;
   const bool rows = a.mode == GART_BACKWARD_GATHER;
-  e = rows ? fill_u8(a.row_flag, 0, a.pair_count, s) : fill_f32(a.acc, 0.0f, a.n * AS, s);
+  e = rows ? fill_u8(a.row_flag, 0, a.pair_count * a.rows_per_pair, s) : fill_f32(a.acc, 0.0f, a.n * AS, s);
   if (e != hipSuccess) return e;
   if ((e = record(a.ev[0], s)) != hipSuccess) return e;
   if (n_tiles > 0) {

@@ -118,9 +118,10 @@ struct BackwardArgs {
   const gart_pixel_state* pixel_state;
   // gradient accumulation
   float* acc;          // [n, acc_stride] per-Gaussian accumulators (atomic modes)
-  float* rows;         // [P, acc_stride] per-pair partial rows (gather mode)
-  uint8_t* row_flag;   // [P] 1 if the pair's row was written
+  float* rows;         // [P * rows_per_pair, acc_stride] partial rows (gather mode)
+  uint8_t* row_flag;   // [P * rows_per_pair] 1 if the row was written
   int64_t pair_count;
+  int32_t rows_per_pair;  // 64-pixel groups per tile (set by the launcher)
   // raw inputs and outputs
   const float* log_scales;
   const float* quats;
