@@ -135,6 +135,10 @@ typedef struct {
   int64_t lt_capacity;    /* number of (L,T) entries allocated */
   gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit */
   gart_pixel_state* pixel_state; /* [height*width] per-pixel end marker (see gart_pixel_state) */
+  uint32_t* hit_list;     /* [pair_capacity * tile^2] composited hits of each pixel, front to back:
+                             for tile t with pairs [b, e) (tile_range), the k-th composited hit of
+                             pixel q of the tile (row-major) is list position (pair - b), stored at
+                             hit_list[tile^2 * (b + k) + q]; k < n_hits <= e - b */
   /* scratch for sorting and gradient accumulation, size from gart_scratch_bytes */
   void* scratch;
   size_t scratch_bytes;
@@ -160,10 +164,10 @@ enum {
   GART_CNT_FWD_TESTS = 1,     /* (pixel, Gaussian) ray tests in the forward */
   GART_CNT_FWD_RESCANS = 2,   /* forward rescans of a tile list (hit-buffer overflow) */
   GART_CNT_BWD_HITS = 3,      /* composited hits visited by the backward */
-  GART_CNT_BWD_TESTS = 4,     /* (pixel, Gaussian) ray tests in the backward */
+  GART_CNT_BWD_TESTS = 4,     /* (pixel, Gaussian) ray tests in the backward (scatter mode) */
   GART_CNT_BWD_ATOMICS = 5,   /* float atomic adds issued by the backward */
   GART_CNT_BWD_PAIRS = 6,     /* (tile, prim) pairs visited by the backward */
-  GART_CNT_BWD_ACTIVE = 7,    /* visited pairs with at least one composited hit */
+  GART_CNT_BWD_ACTIVE = 7,    /* (pair, 64-pixel group) units with a composited hit (gather) */
   GART_CNT_FWD_DROPS = 8,     /* forward hits dropped from a full hit buffer (found again by a rescan) */
   GART_NUM_COUNTERS = 16
 };
@@ -230,7 +234,10 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
  * transmittance in front of the hit, L in the frame's fixed point -- with idx(i,t,p) = O_prim(i) +
  * O_tile(i,t) + O_pixel(i,t,p) (Eq. 16): tiles of the rectangle in
  * row-major order, pixels row-major inside each tile.  Entries for
- * pixels that are not composited hits are left untouched.
+ * pixels that are not composited hits are left untouched.  hit_list
+ * records the pair of every composited hit per pixel (entries past a
+ * pixel's n_hits are left untouched), so that the gather backward reads
+ * which hits to visit instead of re-testing rays.
  * image: [height,width,3] float32, written for every pixel.
  * pixel_state (end marker, final colour in fixed point, final
  * transmittance) is written for every pixel.
@@ -243,13 +250,13 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
  * g_log_scales [n,3], g_quats [n,4] (w.r.t. the unnormalised input
  * quaternion), g_logits [n] and g_sh [n,K,3].
  * settings->backward_mode:
- *   GATHER: one workgroup per tile; lane j owns pairs j, j+B, ... of the
- *     tile list, walks the pixels of rect cap tile, re-tests the ray,
- *     reads (L,T) from the intermediate buffer for composited hits and
- *     accumulates the Gaussian's gradient in registers; each pair writes
- *     one partial row and a per-Gaussian reduction sums its rows and
- *     applies the chain rule.  Deterministic.
- *   GATHER_ATOMIC: as GATHER, but each pair adds its partial into
+ *   GATHER: one workgroup per tile; each lane owns a (pair, 64-pixel
+ *     group) unit of the tile list, walks the unit's composited hits (from
+ *     hit_list), reads (L,T) from the intermediate buffer and accumulates
+ *     the Gaussian's gradient in registers; each unit writes one partial
+ *     row and a per-Gaussian reduction sums its rows and applies the chain
+ *     rule.  Deterministic.
+ *   GATHER_ATOMIC: as GATHER, but each unit adds its partial into
  *     per-Gaussian accumulators with one atomic update per value.
  *   SCATTER: the pixel-centric control (Sec. 3.5): one lane per pixel, one
  *     atomic add per gradient value per composited hit.

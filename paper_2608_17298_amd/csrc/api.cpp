@@ -299,6 +299,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   GART_REQUIRE(image != nullptr && f->pixel_state != nullptr, "image/pixel_state is NULL");
   GART_REQUIRE(f->lt_entries <= f->lt_capacity, "lt capacity");
   GART_REQUIRE(f->lt_entries == 0 || (f->lt != nullptr && aligned16(f->lt)), "lt must be non-NULL, 16-byte aligned");
+  GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
   hipStream_t s = static_cast<hipStream_t>(stream);
   ForwardArgs A{};
   A.cam = make_cam(camera);
@@ -317,6 +318,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.inv_color_step = 1.0 / f->color_step;
   A.image = image;
   A.pixel_state = f->pixel_state;
+  A.hit_list = f->hit_list;
   A.counters = f->counters;
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
@@ -337,6 +339,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(f->stage >= 3, "gart_forward must succeed on this frame first");
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
+  GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
   if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
   const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode, settings->tile);
@@ -364,6 +367,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.color_step = float(f->color_step);
   A.dl_dimage = dL_dimage;
   A.pixel_state = f->pixel_state;
+  A.hit_list = f->hit_list;
   A.acc = at<float>(f->scratch, L.acc);
   A.rows = at<float>(f->scratch, L.rows);
   A.row_flag = at<uint8_t>(f->scratch, L.row_flag);

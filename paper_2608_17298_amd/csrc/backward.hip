@@ -37,7 +37,8 @@ template <int K>
 __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], double sigma, const float sh[3 * K],
                                              const float Y[K], const uint32_t Cq[3], const float g[3], uint4 lt,
                                              float step, float acc[acc_width(K)]) {
-  const float rho = expf(float(-0.5 * D2));
+  // exp(-D2 / 2) as 2^(-D2 log2(e) / 2) on the hardware exp2 (about 1 ulp)
+  const float rho = __builtin_amdgcn_exp2f(float(-0.72134752044448170368 * D2));
   const float a = float(sigma) * rho;
   float c[3];
   bool pos[3];
@@ -52,7 +53,7 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
   const float T = __uint_as_float(lt.w);
   const uint32_t Lq[3] = {lt.x, lt.y, lt.z};
   const float ta = T * a;
-  const float inv = 1.0f / (1.0f - a);
+  const float inv = __builtin_amdgcn_rcpf(1.0f - a);  // about 1 ulp
   float dlda = 0.0f;
   float dc[3];
 #pragma unroll
@@ -83,25 +84,25 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
 // ---------------------------------------------------------------------------
 // Gather: one workgroup per tile.  The tile's pixels form G = TILE^2 / 64
 // groups of 64 pixels (whole rows, one wave each); the unit of work is a
-// (pair, group): the pixels of one group that one Gaussian's rectangle
-// covers.  Per tile:
-//  1. Per-pixel state (ray direction, end marker, SH basis, colour and
-//     upstream gradient) is staged in LDS.  Each group's pixels are ranked
-//     by their ray end, so that "the pixels whose ray ends at or behind
-//     depth k" is one of 65 prefix masks, found by a binary search.
-//  2. Only pairs whose depth bound lies in front of the tile's last ray end
-//     are visited (a prefix of the depth-ordered list), in LDS passes of up
-//     to kUnits units.
-//  3. Candidates, without a ray test: the unit's rectangle rows and columns
-//     AND the pixels whose ray ends at or behind the pair's depth bound.
-//  4. Phase 1: each lane tests the candidate pixels of one unit and keeps
-//     the mask of composited hits.  Units are dealt in order of candidate
-//     count, so the lanes of a round run loops of equal length.
-//  5. Phase 2: each lane accumulates the gradient of one unit's composited
-//     hits in registers (units dealt in order of hit count) and writes one
-//     partial row (or adds it atomically).
+// (pair, group): the composited hits of one Gaussian in one group.  Per tile:
+//  1. Per-pixel state (ray direction, SH basis, final colour and upstream
+//     gradient) is staged in LDS.
+//  2. The tile's pairs are taken in LDS passes of up to kUnits units.  Each
+//     pixel walks the list of its composited hits that the forward recorded
+//     and sets its bit in the 64-bit mask of the unit it belongs to (LDS
+//     atomics).  Units without a composited hit are dropped, the rest are
+//     dealt to lanes in order of hit count, so the lanes of a round run
+//     loops of similar length.
+//  3. Each lane accumulates the gradient of one unit's hits in registers and
+//     writes one partial row (or adds it atomically).
 // ---------------------------------------------------------------------------
 constexpr int kUnits = 512;  // units per LDS pass
+
+// Per-pixel ray direction in LDS, padded to 32 bytes.
+struct __align__(16) RayRec {
+  double d[3];
+  double pad;
+};
 
 // Deals the units of a pass by bucket (0 first; 0xff = dropped): counting
 // sort into s_order.  s_hist holds the bucket counts on entry and is zero on
@@ -141,22 +142,15 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   constexpr int kPairs = kUnits / G;
   constexpr int AW = acc_width(K), AS = acc_stride(K);
   constexpr int KP = (K + 3) & ~3;  // SH basis row padded to 16 bytes
-  constexpr double kInf = __builtin_huge_val();
-  // one bit per row start of a group: rows r = 0..R-1 at bit r * TILE
-  constexpr uint64_t kRowOnes = TILE == 8 ? 0x0101010101010101ull : 0x0001000100010001ull;
   static_assert(NT % 64 == 0 && (TILE == 8 || TILE == 16), "tile of 8 or 16");
 
-  __shared__ double4 s_ray[NT];                 // d.xyz, tau_end
-  __shared__ uint32_t s_iend[NT];
+  __shared__ RayRec s_ray[NT];
   __shared__ __align__(16) float s_Y[NT][KP];
-  __shared__ __align__(16) float s_cg[NT][8];   // C.rgb (fixed-point bits), g.rgb
-  __shared__ double s_tsort[G][64];             // ray ends of a group, descending
-  __shared__ uint32_t s_pix[G][64];             // pixel of each rank
-  __shared__ uint64_t s_prefix[G][65];          // pixels of the k latest ray ends
-  __shared__ double s_wmax[G];
-  __shared__ uint32_t s_red[G];
+  __shared__ __align__(16) float s_cg[NT][8];  // C.rgb (fixed-point bits), g.rgb
   __shared__ uint32_t s_hist[64];
   __shared__ uint32_t s_total;
+  __shared__ double s_wmax[G];
+  __shared__ uint32_t s_red[G];
   __shared__ uint64_t s_mask[kUnits];
   __shared__ uint32_t s_id[kPairs];
   __shared__ uint8_t s_bucket[kUnits];
@@ -167,9 +161,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
   const int ox = tx * TILE, oy = ty * TILE;
   const int tid = threadIdx.x;
-  const int wv = tid / 64, lane = tid % 64;
-
-  double my_tend;
+  uint32_t my_hits = 0;  // composited hits of this thread's pixel
   {
     const int px = ox + tid % TILE, py = oy + tid / TILE;
     const bool valid = px < A.cam.W && py < A.cam.H;
@@ -179,60 +171,39 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
 #pragma unroll
     for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
-    double tend = -kInf;  // a pixel outside the image is never a candidate
-    uint32_t iend = 0;
     uint32_t cq[3] = {0, 0, 0};
     float gg[3] = {0, 0, 0};
+    double tend = -__builtin_huge_val();
     if (valid) {
       const int64_t p = int64_t(py) * A.cam.W + px;
 #pragma unroll
-      for (int ch = 0; ch < 3; ++ch) gg[ch] = A.dl_dimage[3 * p + ch];
-      const gart_pixel_state st = A.pixel_state[p];
-      tend = st.tau_end;
-      iend = st.id_end;
-#pragma unroll
-      for (int ch = 0; ch < 3; ++ch) cq[ch] = st.color_fixed[ch];
+      for (int ch = 0; ch < 3; ++ch) {
+        gg[ch] = A.dl_dimage[3 * p + ch];
+        cq[ch] = A.pixel_state[p].color_fixed[ch];
+      }
+      my_hits = A.pixel_state[p].n_hits;
+      tend = A.pixel_state[p].tau_end;
     }
-    s_ray[tid] = make_double4(d[0], d[1], d[2], tend);
-    s_iend[tid] = iend;
+    RayRec rr;
+    rr.d[0] = d[0];
+    rr.d[1] = d[1];
+    rr.d[2] = d[2];
+    rr.pad = 0.0;
+    s_ray[tid] = rr;
     *reinterpret_cast<uint4*>(&s_cg[tid][0]) = make_uint4(cq[0], cq[1], cq[2], __float_as_uint(gg[0]));
     *reinterpret_cast<float4*>(&s_cg[tid][4]) = make_float4(gg[1], gg[2], 0.0f, 0.0f);
     double m = tend;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
-    if (lane == 0) s_wmax[wv] = m;
-    my_tend = tend;
+    if (tid % 64 == 0) s_wmax[tid / 64] = m;
   }
   __syncthreads();
-  {
-    // Rank of this pixel's ray end within its group (latest first, ties by
-    // pixel), then prefix masks by rank.
-    int rank = 0;
-    for (int q = 0; q < 64; ++q) {
-      const double t = s_ray[wv * 64 + q].w;
-      rank += (t > my_tend || (t == my_tend && q < lane)) ? 1 : 0;
-    }
-    s_tsort[wv][rank] = my_tend;
-    s_pix[wv][rank] = uint32_t(lane);
-  }
-  __syncthreads();
-  {
-    uint64_t pm = 1ull << s_pix[wv][lane];
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint64_t u = __shfl_up(pm, off);
-      if (lane >= off) pm |= u;
-    }
-    s_prefix[wv][lane + 1] = pm;
-    if (lane == 0) s_prefix[wv][0] = 0;
-    if (tid < 64) s_hist[tid] = 0;
-  }
   double tmax = s_wmax[0];
 #pragma unroll
   for (int w = 1; w < G; ++w) tmax = fmax(tmax, s_wmax[w]);
 
-  // Number of visited pairs: the list is ordered by depth bound, so they
-  // form its prefix of pairs whose bound is <= tmax.
+  // Only the prefix of the depth-ordered list whose depth bound lies in front
+  // of the tile's last ray end can hold composited hits.
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
   uint32_t nv = 0;
   for (int64_t j = beg + tid; j < end; j += NT) {
@@ -241,81 +212,51 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) nv += __shfl_xor(nv, off);
-  if (lane == 0) s_red[wv] = nv;
+  if (tid % 64 == 0) s_red[tid / 64] = nv;
   __syncthreads();
-  int64_t V = 0;
+  int64_t vend = beg;
 #pragma unroll
-  for (int w = 0; w < G; ++w) V += s_red[w];
+  for (int w = 0; w < G; ++w) vend += s_red[w];
 
-  uint32_t n_pairs = 0, n_hits = 0, n_tests = 0, n_atom = 0, n_active = 0;
-  for (int64_t c0 = 0; c0 < V; c0 += kPairs) {
-    const int nc = int(min<int64_t>(kPairs, V - c0));
+  uint32_t n_pairs = 0, n_hits = 0, n_atom = 0, n_active = 0;
+  for (int64_t c0 = beg; c0 < vend; c0 += kPairs) {
+    const int nc = int(min<int64_t>(kPairs, vend - c0));
     const int nu = nc * G;
-    // Candidates of every unit of the pass.
+    for (int u = tid; u < nu; u += NT) s_mask[u] = 0;
     for (int q = tid; q < nc; q += NT) {
-      const uint32_t i = A.pair_prim[beg + c0 + q];
-      s_id[q] = i;
+      s_id[q] = A.pair_prim[c0 + q];
       ++n_pairs;
-      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
-      const double key = A.geom[int64_t(kGeomStride) * i + kGeoKey];
-      const int xa = max(r.x, ox), xb = min(r.z, ox + TILE - 1);
-      const uint64_t cols = ((1ull << (xb - xa + 1)) - 1ull) << (xa - ox);
+    }
+    if (tid < 64) s_hist[tid] = 0;
+    __syncthreads();
+    // This pixel's composited hits whose pair lies in the pass (list loads
+    // issued eight at a time).
+    {
+      const uint32_t lo = uint32_t(c0 - beg);
+      const uint32_t* hl = A.hit_list + int64_t(NT) * beg + tid;
+      const uint64_t bit = 1ull << (tid % 64);
+      uint32_t k = 0;
+      for (; k + 8 <= my_hits; k += 8) {
+        uint32_t q[8];
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const int gy0 = oy + g * R;
-        const int ya = max(r.y, gy0), yb = min(r.w, gy0 + R - 1);
-        uint64_t m = 0;
-        if (ya <= yb) {
-          const uint64_t rows = (kRowOnes >> ((R - 1 - (yb - ya)) * TILE)) << ((ya - gy0) * TILE);
-          int lo = 0, hi = 64;  // number of pixels whose ray ends at or behind key
-          while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (s_tsort[g][mid] >= key)
-              lo = mid + 1;
-            else
-              hi = mid;
-          }
-          m = cols * rows & s_prefix[g][lo];
-        }
-        const int u = q * G + g;
-        s_mask[u] = m;
-        const int c = __popcll(m);
-        s_bucket[u] = c ? uint8_t(64 - c) : uint8_t(0xff);
-        if (c) atomicAdd(&s_hist[64 - c], 1u);
+        for (int t = 0; t < 8; ++t) q[t] = hl[int64_t(NT) * (k + t)] - lo;
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (q[t] < uint32_t(nc)) atomicOr(&s_mask[q[t] * G + tid / 64], bit);
+      }
+      for (; k < my_hits; ++k) {
+        const uint32_t q = hl[int64_t(NT) * k] - lo;
+        if (q < uint32_t(nc)) atomicOr(&s_mask[q * G + tid / 64], bit);
       }
     }
-    const int nu1 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total);
-
-    // Phase 1: ray tests of the candidates -> mask of composited hits.
-    for (int o = tid; o < nu1; o += NT) {
-      const int u = s_order[o], g = u % G;
-      const uint32_t i = s_id[u / G];
-      const double* Gm = A.geom + int64_t(kGeomStride) * i;
-      double W[9], og[3];
-#pragma unroll
-      for (int k = 0; k < 9; ++k) W[k] = Gm[k];
-#pragma unroll
-      for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
-      const double D2c = Gm[kGeoD2c];
-      uint64_t m = s_mask[u], hit = 0;
-      while (m) {
-        const int b = __builtin_ctzll(m);
-        m &= m - 1;
-        const int lp = g * 64 + b;
-        const double4 ry = s_ray[lp];
-        const double d[3] = {ry.x, ry.y, ry.z};
-        double tau, D2, xg[3];
-        ++n_tests;
-        if (ray_hit(W, og, D2c, d, &tau, &D2, xg) && !key_less(ry.w, s_iend[lp], tau, i)) hit |= 1ull << b;
-      }
-      s_mask[u] = hit;
-      const int c = __popcll(hit);
+    __syncthreads();
+    for (int u = tid; u < nu; u += NT) {
+      const int c = __popcll(s_mask[u]);
       s_bucket[u] = c ? uint8_t(64 - c) : uint8_t(0xff);
       if (c) atomicAdd(&s_hist[64 - c], 1u);
     }
     const int nu2 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total);
 
-    // Phase 2: gradient of each unit's composited hits, in row-major order.
     for (int o = tid; o < nu2; o += NT) {
       const int u = s_order[o], g = u % G;
       const uint32_t i = s_id[u / G];
@@ -325,7 +266,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       for (int k = 0; k < 9; ++k) W[k] = Gm[k];
 #pragma unroll
       for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
-      const double D2c = Gm[kGeoD2c], sigma = Gm[kGeoSigma];
+      const double sigma = Gm[kGeoSigma];
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
       float sh[3 * K];
       const float* shp = A.sh + int64_t(i) * (3 * K);
@@ -342,6 +283,8 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       float acc[AW];
 #pragma unroll
       for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
+      // Composited hits in row-major order; each (L,T) entry is loaded one hit
+      // ahead of its use.
       uint64_t m = s_mask[u];
       int b = __builtin_ctzll(m);
       uint4 lt_next = lt_at(b);
@@ -351,10 +294,8 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
         const int bn = m ? __builtin_ctzll(m) : b;
         if (m) lt_next = lt_at(bn);
         const int lp = g * 64 + b;
-        const double4 ry = s_ray[lp];
-        const double d[3] = {ry.x, ry.y, ry.z};
-        double tau, D2, xg[3];
-        ray_hit(W, og, D2c, d, &tau, &D2, xg);
+        double D2, xg[3];
+        hit_point(W, og, s_ray[lp].d, &D2, xg);
         ++n_hits;
         float Y[KP];
 #pragma unroll
@@ -400,7 +341,6 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     count_add(A.counters + GART_CNT_BWD_PAIRS, n_pairs);
     count_add(A.counters + GART_CNT_BWD_ACTIVE, n_active);
     count_add(A.counters + GART_CNT_BWD_HITS, n_hits);
-    count_add(A.counters + GART_CNT_BWD_TESTS, n_tests);
     count_add(A.counters + GART_CNT_BWD_ATOMICS, n_atom);
   }
 }

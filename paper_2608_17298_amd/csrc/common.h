@@ -70,6 +70,26 @@ __device__ __forceinline__ bool ray_hit(const double W[9], const double og[3], d
   return tau > 0.0 && D2 <= D2c;
 }
 
+// Closest-approach point x_g and D^2 there for a ray already known to hit,
+// for gradient evaluation only (never for a decision): tau uses the hardware
+// reciprocal refined by two Newton steps instead of a correctly rounded
+// division.
+__device__ __forceinline__ void hit_point(const double W[9], const double og[3], const double d[3], double* D2_out,
+                                          double xg[3]) {
+  double dg[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) dg[k] = fma(W[3 * k], d[0], fma(W[3 * k + 1], d[1], W[3 * k + 2] * d[2]));
+  const double num = fma(og[0], dg[0], fma(og[1], dg[1], og[2] * dg[2]));
+  const double den = fma(dg[0], dg[0], fma(dg[1], dg[1], dg[2] * dg[2]));
+  double r = __builtin_amdgcn_rcp(den);
+  r = fma(r, fma(-den, r, 1.0), r);
+  r = fma(r, fma(-den, r, 1.0), r);
+  const double tau = -num * r;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) xg[k] = fma(tau, dg[k], og[k]);
+  *D2_out = fma(xg[0], xg[0], fma(xg[1], xg[1], xg[2] * xg[2]));
+}
+
 // (tau, id) lexicographic order used to composite hits.
 __device__ __forceinline__ bool key_less(double t1, uint32_t i1, double t2, uint32_t i2) {
   return t1 < t2 || (t1 == t2 && i1 < i2);

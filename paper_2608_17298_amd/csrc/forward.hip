@@ -119,6 +119,9 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     }
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) c[ch] = fmaxf(c[ch], 0.0f);
+    // k-th composited hit of this pixel -> its list position (read by the
+    // gather backward)
+    A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = bc[0];
     A.lt[lt_base + bi[0]] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
                                        color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
     const double w = T * a;

@@ -93,6 +93,7 @@ struct ForwardArgs {
   double inv_color_step;    // fixed-point units per unit of colour
   float* image;
   gart_pixel_state* pixel_state;
+  uint32_t* hit_list;       // [pairs * tile^2] list position of each pixel's k-th composited hit
   uint64_t* counters;
   void* ev_begin;  // optional hipEvent_t recorded around the kernel
   void* ev_end;
@@ -116,6 +117,7 @@ struct BackwardArgs {
   float color_step;         // colour per fixed-point unit (a power of two times a float)
   const float* dl_dimage;
   const gart_pixel_state* pixel_state;
+  const uint32_t* hit_list;  // [pairs * tile^2] list position of each pixel's k-th composited hit
   // gradient accumulation
   float* acc;          // [n, acc_stride] per-Gaussian accumulators (atomic modes)
   float* rows;         // [P * rows_per_pair, acc_stride] partial rows (gather mode)

@@ -63,7 +63,7 @@ class gart_settings(ctypes.Structure):
 class gart_frame(ctypes.Structure):
     _fields_ = [("rect", _P), ("lt_offset", _P), ("prim_geom", _P), ("tile_count", _P),
                 ("pair_offset", _P), ("pair_capacity", ctypes.c_int64), ("pair_tile", _P), ("pair_prim", _P),
-                ("tile_range", _P), ("lt_capacity", ctypes.c_int64), ("lt", _P), ("pixel_state", _P),
+                ("tile_range", _P), ("lt_capacity", ctypes.c_int64), ("lt", _P), ("pixel_state", _P), ("hit_list", _P),
                 ("scratch", _P), ("scratch_bytes", ctypes.c_size_t), ("counters", _P),
                 ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
@@ -237,6 +237,8 @@ class Frame:
         cap = int(cap)
         self.pair_tile = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
         self.pair_prim = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
+        # composited-hit lists: tile^2 slots per pair (see gart_frame.hit_list)
+        self.hit_list = torch.empty(max(cap, 1) * self.settings.tile ** 2, dtype=torch.int32, device=self.device)
         self.pair_capacity = cap
         # sized for every backward mode, so one frame serves all of them
         nbytes = 0
@@ -250,7 +252,7 @@ class Frame:
             self.lt = None
             self._alloc_lt(int(lt_entries * slack) + 1)
         if pair_count > self.pair_capacity:
-            self.pair_tile = self.pair_prim = self.scratch = None
+            self.pair_tile = self.pair_prim = self.hit_list = self.scratch = None
             self._alloc_pairs(int(pair_count * slack) + 1)
 
     def c_struct(self) -> gart_frame:
@@ -260,7 +262,7 @@ class Frame:
         f.pair_capacity = self.pair_capacity
         f.pair_tile, f.pair_prim, f.tile_range = _ptr(self.pair_tile), _ptr(self.pair_prim), _ptr(self.tile_range)
         f.lt_capacity = self.lt_capacity
-        f.lt, f.pixel_state = _ptr(self.lt), _ptr(self.pixel_state)
+        f.lt, f.pixel_state, f.hit_list = _ptr(self.lt), _ptr(self.pixel_state), _ptr(self.hit_list)
         f.scratch, f.scratch_bytes = _ptr(self.scratch), self.scratch.numel()
         f.counters = _ptr(self.counters)
         for k in range(NUM_EVENTS):
