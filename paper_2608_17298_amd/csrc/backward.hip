@@ -97,6 +97,7 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
 //     writes one partial row (or adds it atomically).
 // ---------------------------------------------------------------------------
 constexpr int kUnits = 512;  // units per LDS pass
+constexpr int kBatch = 4;    // composited hits whose (L,T) loads are issued together
 
 // Per-pixel ray direction in LDS, padded to 32 bytes.
 struct __align__(16) RayRec {
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   __shared__ uint16_t s_order[kUnits];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
-  const int tile = xcd_tile(blockIdx.x, n_tiles);
+  const int tile = xcd_tile(blockIdx.x, n_tiles, A.tiles_x);
   const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
   const int ox = tx * TILE, oy = ty * TILE;
   const int tid = threadIdx.x;
@@ -283,35 +284,46 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       float acc[AW];
 #pragma unroll
       for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
-      // Composited hits in row-major order; each (L,T) entry is loaded one hit
-      // ahead of its use.
+      // Composited hits in row-major order, in batches of kBatch: the batch's
+      // (L,T) loads are all issued before its first hit is evaluated, so one
+      // memory latency is paid per batch (no load is pending across
+      // iterations, which would make the compiler wait for it early).
       uint64_t m = s_mask[u];
-      int b = __builtin_ctzll(m);
-      uint4 lt_next = lt_at(b);
       while (m) {
-        const uint4 lt = lt_next;
-        m &= m - 1;
-        const int bn = m ? __builtin_ctzll(m) : b;
-        if (m) lt_next = lt_at(bn);
-        const int lp = g * 64 + b;
-        double D2, xg[3];
-        hit_point(W, og, s_ray[lp].d, &D2, xg);
-        ++n_hits;
-        float Y[KP];
+        int bb[kBatch];
+        uint4 lv[kBatch];
 #pragma unroll
-        for (int kk = 0; kk < KP; kk += 4) {
-          const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[lp][kk]);
-          Y[kk] = y4.x;
-          Y[kk + 1] = y4.y;
-          Y[kk + 2] = y4.z;
-          Y[kk + 3] = y4.w;
+        for (int t = 0; t < kBatch; ++t) {
+          bb[t] = m ? __builtin_ctzll(m) : -1;
+          if (m) {
+            m &= m - 1;
+            lv[t] = lt_at(bb[t]);
+          } else {
+            lv[t] = make_uint4(0, 0, 0, 0);
+          }
         }
-        const uint4 c4 = *reinterpret_cast<const uint4*>(&s_cg[lp][0]);
-        const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
-        const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
-        const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
-        hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, gr, lt, A.color_step, acc);
-        b = bn;
+#pragma unroll
+        for (int t = 0; t < kBatch; ++t) {
+          if (bb[t] < 0) break;
+          const int lp = g * 64 + bb[t];
+          double D2, xg[3];
+          hit_point(W, og, s_ray[lp].d, &D2, xg);
+          ++n_hits;
+          float Y[KP];
+#pragma unroll
+          for (int kk = 0; kk < KP; kk += 4) {
+            const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[lp][kk]);
+            Y[kk] = y4.x;
+            Y[kk + 1] = y4.y;
+            Y[kk + 2] = y4.z;
+            Y[kk + 3] = y4.w;
+          }
+          const uint4 c4 = *reinterpret_cast<const uint4*>(&s_cg[lp][0]);
+          const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
+          const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
+          const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
+          hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
+        }
       }
       ++n_active;
       if constexpr (ATOMIC) {
@@ -357,7 +369,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
   __shared__ __align__(16) double s_row[NT * kRow];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
-  const int tile = xcd_tile(blockIdx.x, n_tiles);
+  const int tile = xcd_tile(blockIdx.x, n_tiles, A.tiles_x);
   const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
   const int tid = threadIdx.x;
   const int px = tx * TILE + tid % TILE, py = ty * TILE + tid / TILE;

@@ -136,14 +136,24 @@ __device__ __forceinline__ int64_t lt_local_index(int x0, int y0, int x1, int y1
   return o_tile + o_pix;
 }
 
-// Block index -> tile index such that each of the 8 XCDs (which receive
-// blocks round-robin) works on one contiguous band of tiles and keeps the
-// band's Gaussians in its own L2.
-__device__ __forceinline__ int xcd_tile(int b, int n) {
-  const int q = n / 8, r = n % 8;
-  const int x = b % 8, k = b / 8;
-  // XCD x owns tiles [x*q + min(x, r), ...) of length q + (x < r)
-  return x * q + min(x, r) + k;
+// Block index -> tile index.  Blocks reach the 8 XCDs round-robin; each
+// XCD receives patches of 4x2 neighbouring tiles (which share Gaussians in
+// its L2), and consecutive patches go to different XCDs, so that every XCD
+// gets a share of the dense and of the sparse parts of the image.  tiles_x
+// is the tile grid width.  A bijection of [0, n).
+__device__ __forceinline__ int xcd_tile(int b, int n, int tiles_x) {
+  // blocks 64a + r, r = 8 q + x (XCD x): patch slot 8 x + q of group a
+  int i = b;
+  if (b < (n / 64) * 64) {
+    const int r = b % 64;
+    i = (b - r) + 8 * (r % 8) + r / 8;
+  }
+  // order tiles in bands of two tile rows, column by column inside a band,
+  // so that 8 consecutive indices form a 4x2 patch
+  const int band = i / (2 * tiles_x), k = i % (2 * tiles_x);
+  const int tiles_y_full = (n / tiles_x) & ~1;  // rows covered by complete bands
+  if (2 * band >= tiles_y_full) return i;       // last, single-row band: row-major
+  return (2 * band + k % 2) * tiles_x + k / 2;
 }
 
 __device__ __forceinline__ unsigned lane_id() { return __lane_id(); }

@@ -49,7 +49,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   __shared__ unsigned s_restart;
 
   const int n_tiles = A.tiles_x * A.tiles_y;
-  const int tile = xcd_tile(blockIdx.x, n_tiles);
+  const int tile = xcd_tile(blockIdx.x, n_tiles, A.tiles_x);
   const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
   const int tid = threadIdx.x;
   const int px = tx * TILE + tid % TILE, py = ty * TILE + tid / TILE;
