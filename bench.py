@@ -29,12 +29,18 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
-FP32_PEAK_TFLOPS = 157.3       # MI355X vector FP32
-FP64_PEAK_TFLOPS = 78.6        # MI355X vector FP64
+# Vector ALU peak from the unit counts: 256 CUs x 4 SIMDs x 16 lanes x 2 flops
+# (FMA) x 2.4 GHz = 78.6 TFLOP/s, for fp64 and for fp32 without packed
+# instructions (the library is built without them; the 157.3 TFLOP/s fp32
+# figure counts two packed operations per lane).
+FP32_PEAK_TFLOPS = 78.6
+FP64_PEAK_TFLOPS = 78.6
 
 # Algorithmic cost model (per unit of work).
 F64_PER_TEST = 40              # ray/Gaussian max-response test in fp64 (W d, two dots, tau, x_g, D2, compare)
-GEOM_BYTES = 128 + 16 + 8 + 4  # per visited pair: fp64 geometry row, rect, O_prim, pair index
+F64_PER_HIT_BWD = 45           # gather: x_g and D2 of a composited hit in fp64 (no decision)
+GEOM_BYTES = 128 + 16 + 8 + 4  # per staged pair in the forward: fp64 geometry row, rect, O_prim, pair index
+UNIT_BYTES = 104 + 8 + 16 + 8 + 8  # per gather unit: W and o_g, sigma, rect, O_prim, pair offset
 
 
 def f32_per_hit_bwd(K):
@@ -226,12 +232,18 @@ def main():
     bwd_tests, bwd_hits = int(c[gart.CNT_BWD_TESTS]), int(c[gart.CNT_BWD_HITS])
     bwd_pairs, bwd_active = int(c[gart.CNT_BWD_PAIRS]), int(c[gart.CNT_BWD_ACTIVE])
     fwd_tests = int(c[gart.CNT_FWD_TESTS])
+    # gather: per composited hit its (L,T) entry and hit-list word; per visited
+    # pair its index and depth bound; per (pair, group) unit with hits the
+    # Gaussian's geometry and SH, one partial row and its flag; per pixel the
+    # upstream gradient and pixel state.  forward: per composited hit the
+    # (L,T) entry and hit-list word written; per staged pair its geometry row;
+    # SH once per (tile, Gaussian) with hits; per pixel the image and state.
     work = {
         "backward_main": dict(
-            bytes=16 * bwd_hits + bwd_pairs * (GEOM_BYTES + 12 * K) + bwd_active * (4 * AS + 1) + npix * (12 + 32),
-            f64=F64_PER_TEST * bwd_tests, f32=f32_per_hit_bwd(K) * bwd_hits),
+            bytes=20 * bwd_hits + 12 * bwd_pairs + bwd_active * (UNIT_BYTES + 12 * K + 4 * AS + 1) + npix * (12 + 32),
+            f64=F64_PER_TEST * bwd_tests + F64_PER_HIT_BWD * bwd_hits, f32=f32_per_hit_bwd(K) * bwd_hits),
         "forward_trace": dict(
-            bytes=16 * hits + int(frame.pair_count) * GEOM_BYTES + npix * (12 + 32) + hits * 12 * K,
+            bytes=20 * hits + int(frame.pair_count) * GEOM_BYTES + bwd_active * 12 * K + npix * (12 + 32),
             f64=F64_PER_TEST * fwd_tests + 30 * hits, f32=f32_per_hit_fwd(K) * hits),
     }
 
@@ -299,7 +311,7 @@ def main():
         "forward_rescans": int(c[gart.CNT_FWD_RESCANS]),
         "counters": {name: int(c[i]) for i, name in enumerate(
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
-             "bwd_active_pairs", "fwd_drops"])},
+             "bwd_active_units", "fwd_drops"])},
         "kernels_roofline": {k: roofline(k) for k in work},
     }
     s = json.dumps(line)

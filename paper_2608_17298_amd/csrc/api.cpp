@@ -39,7 +39,7 @@ gart_status fail(gart_status s, const char* fmt, ...) {
 size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t depth_key, key_alt, perm, perm_alt, base_rank, pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals,
+  size_t depth_key, key_alt, perm, perm_alt, base_rank, pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials,
       acc, rows, row_flag, total;
 };
 
@@ -62,6 +62,7 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
   L.radix_tmp = take(radix_tmp_bytes(std::max(nn, pc)));
   L.scan_tmp = take(scan_tmp_bytes(nn + 1));
   L.totals = take(64);
+  L.partials = take(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
   const size_t AS = size_t(acc_stride(K));
   L.acc = take(mode == GART_BACKWARD_GATHER ? 4 : size_t(nn) * AS * 4);
   const size_t rpp = size_t(tile) * size_t(tile) / 64;  // partial rows per pair (64-pixel groups)
@@ -182,9 +183,7 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   f->stage = 0;
-  unsigned long long* pair_total = at<unsigned long long>(f->scratch, L.totals);
-  uint32_t* color_bound = reinterpret_cast<uint32_t*>(pair_total + 1);
-  GART_HIP(fill_u32(reinterpret_cast<uint32_t*>(pair_total), 0u, 3, s));
+  unsigned long long* totals = at<unsigned long long>(f->scratch, L.totals);
   BoundsArgs A{};
   A.means = g->means;
   A.log_scales = g->log_scales;
@@ -201,17 +200,16 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   A.geom = f->prim_geom;
   A.tile_count = f->tile_count;
   A.depth_key = at<uint32_t>(f->scratch, L.depth_key);
-  A.pair_total = pair_total;
-  A.color_bound = color_bound;
+  A.block_partial = at<unsigned long long>(f->scratch, L.partials);
   GART_HIP(launch_bounds(A, s));
   GART_HIP(scan_exclusive_i64(f->lt_offset, f->lt_offset, n, f->lt_offset + n, at<void>(f->scratch, L.scan_tmp), s));
-  int64_t host[2] = {0, 0};
-  GART_HIP(hipMemcpyAsync(&host[0], f->lt_offset + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-  GART_HIP(hipMemcpyAsync(&host[1], pair_total, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-  uint32_t cb_bits = 0;
-  GART_HIP(hipMemcpyAsync(&cb_bits, color_bound, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  GART_HIP(launch_bounds_totals(A.block_partial, (n + kBoundsBlock - 1) / kBoundsBlock, f->lt_offset + n, totals, s));
+  unsigned long long tot[3] = {0, 0, 0};  // (L,T) entries, pairs, colour bound bits
+  GART_HIP(hipMemcpyAsync(tot, totals, sizeof tot, hipMemcpyDeviceToHost, s));
   GART_HIP(hipStreamSynchronize(s));
+  const int64_t host[2] = {int64_t(tot[0]), int64_t(tot[1])};
   float cb;
+  const uint32_t cb_bits = uint32_t(tot[2]);
   std::memcpy(&cb, &cb_bits, sizeof cb);
   f->color_step = double(cb > 0.0f ? cb : 1.0f) / 4294967296.0;
 

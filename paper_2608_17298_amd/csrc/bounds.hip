@@ -74,7 +74,8 @@ __device__ bool axis_cover(double Qaa, double Qa4, double Q44, int npix, int* lo
   return true;
 }
 
-__global__ __launch_bounds__(256) void bounds_kernel(BoundsArgs A) {
+template <int K>
+__global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   uint32_t my_tiles = 0;
   float my_cb = 0.0f;
@@ -205,32 +206,87 @@ __global__ __launch_bounds__(256) void bounds_kernel(BoundsArgs A) {
     if (my_tiles) {
       // Colour bound over all directions: per band l, |sum_m sh_lm Y_lm| <=
       // |sh_l| sqrt((2l+1)/(4 pi)) (Cauchy-Schwarz and the addition theorem).
-      // Rounded up generously so that the fp32 evaluation of the colour in
-      // the forward stays below it.
-      const float* sp = A.sh + int64_t(3) * A.K * i;
-      double cb = 0.0;
+      // fp32 with a margin of 2^-16 (far above the rounding of this sum and
+      // of the forward's fp32 colour); the fixed-point conversion saturates
+      // in any case.
+      // all 3K coefficients are loaded before use (wide loads, each line
+      // fetched once)
+      const float* sp = A.sh + int64_t(3 * K) * i;
+      float c[3 * K];
+#pragma unroll
+      for (int k = 0; k < 3 * K; ++k) c[k] = sp[k];
+      float ss[4][3] = {};
+      constexpr int kBand[16] = {0, 1, 1, 1, 2, 2, 2, 2, 2, 3, 3, 3, 3, 3, 3, 3};
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) ss[kBand[k]][ch] = fmaf(c[3 * k + ch], c[3 * k + ch], ss[kBand[k]][ch]);
+      float cb = 0.0f;
+#pragma unroll
       for (int ch = 0; ch < 3; ++ch) {
-        double v = 0.5;
-        for (int l = 0; l * l < A.K; ++l) {
-          double ss = 0.0;
-          for (int k = l * l; k < (l + 1) * (l + 1); ++k) ss += double(sp[3 * k + ch]) * double(sp[3 * k + ch]);
-          v += sqrt(ss * double(2 * l + 1) / (4.0 * 3.14159265358979323846));
-        }
-        cb = fmax(cb, v);
+        float v = 0.5f;
+#pragma unroll
+        for (int l = 0; l < 4; ++l) v += sqrtf(ss[l][ch] * (float(2 * l + 1) * 0.07957747154594767f));
+        cb = fmaxf(cb, v);
       }
-      my_cb = float(cb * (1.0 + 1.0 / 65536.0));
+      my_cb = cb * (1.0f + 1.0f / 65536.0f);
       if (!(my_cb >= 0.0f && my_cb < 1e30f)) my_cb = 1e30f;  // non-finite SH: saturate
     }
   }
-  // block sum of tile counts and max of colour bounds -> one atomic per wave
+  // block sum of tile counts and max of colour bounds -> one partial per block
+  __shared__ unsigned long long s_t[kBoundsBlock / 64];
+  __shared__ float s_cb[kBoundsBlock / 64];
   unsigned long long t = my_tiles;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
     t += __shfl_xor(t, off);
     my_cb = fmaxf(my_cb, __shfl_xor(my_cb, off));
   }
-  if (__lane_id() == 0 && t) atomicAdd(A.pair_total, t);
-  if (__lane_id() == 0 && my_cb > 0.0f) atomicMax(A.color_bound, __float_as_uint(my_cb));
+  if (__lane_id() == 0) {
+    s_t[threadIdx.x / 64] = t;
+    s_cb[threadIdx.x / 64] = my_cb;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kBoundsBlock / 64; ++w) {
+      t += s_t[w];
+      my_cb = fmaxf(my_cb, s_cb[w]);
+    }
+    A.block_partial[2 * blockIdx.x] = t;
+    A.block_partial[2 * blockIdx.x + 1] = __float_as_uint(my_cb);
+  }
+}
+
+__global__ __launch_bounds__(256) void bounds_totals_kernel(const unsigned long long* __restrict__ part, int64_t nb,
+                                                            const int64_t* __restrict__ area_total,
+                                                            unsigned long long* __restrict__ totals) {
+  __shared__ unsigned long long s_t[4];
+  __shared__ float s_cb[4];
+  unsigned long long t = 0;
+  float cb = 0.0f;
+  for (int64_t b = threadIdx.x; b < nb; b += 256) {
+    t += part[2 * b];
+    cb = fmaxf(cb, __uint_as_float(uint32_t(part[2 * b + 1])));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    t += __shfl_xor(t, off);
+    cb = fmaxf(cb, __shfl_xor(cb, off));
+  }
+  if (__lane_id() == 0) {
+    s_t[threadIdx.x / 64] = t;
+    s_cb[threadIdx.x / 64] = cb;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w) {
+      t += s_t[w];
+      cb = fmaxf(cb, s_cb[w]);
+    }
+    totals[0] = static_cast<unsigned long long>(*area_total);
+    totals[1] = t;
+    totals[2] = __float_as_uint(cb);
+  }
 }
 
 __global__ void gather_counts_kernel(TileMapArgs A) {
@@ -295,7 +351,20 @@ __global__ void tile_ranges_kernel(const uint32_t* __restrict__ keys, int64_t m,
 
 hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  bounds_kernel<<<ceil_div(a.n, 256), 256, 0, s>>>(a);
+  const int64_t nb = ceil_div(a.n, kBoundsBlock);
+  switch (a.K) {
+    case 1: bounds_kernel<1><<<nb, kBoundsBlock, 0, s>>>(a); break;
+    case 4: bounds_kernel<4><<<nb, kBoundsBlock, 0, s>>>(a); break;
+    case 9: bounds_kernel<9><<<nb, kBoundsBlock, 0, s>>>(a); break;
+    case 16: bounds_kernel<16><<<nb, kBoundsBlock, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bounds_totals(const unsigned long long* block_partial, int64_t n_blocks, const int64_t* area_total,
+                                unsigned long long* totals, hipStream_t s) {
+  bounds_totals_kernel<<<1, 256, 0, s>>>(block_partial, n_blocks, area_total, totals);
   return hipGetLastError();
 }
 

@@ -54,10 +54,16 @@ struct BoundsArgs {
   double* geom;
   uint32_t* tile_count;
   uint32_t* depth_key;      // [n] float bits of the depth lower bound
-  unsigned long long* pair_total;  // device accumulator of sum tile_count
-  uint32_t* color_bound;    // float bits, max over visible Gaussians of the colour bound
+  // per block of kBoundsBlock Gaussians: [2b] sum of tile counts, [2b+1]
+  // max colour bound (float bits); reduced by launch_bounds_totals
+  unsigned long long* block_partial;
 };
+constexpr int kBoundsBlock = 256;
 hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s);
+// totals[0] = *area_total, totals[1] = sum of the pair partials, totals[2] =
+// max of the colour partials (float bits; 0 if no visible Gaussian)
+hipError_t launch_bounds_totals(const unsigned long long* block_partial, int64_t n_blocks, const int64_t* area_total,
+                                unsigned long long* totals, hipStream_t s);
 
 struct TileMapArgs {
   int64_t n;
