@@ -97,7 +97,7 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
 //     writes one partial row (or adds it atomically).
 // ---------------------------------------------------------------------------
 constexpr int kUnits = 512;  // units per LDS pass
-constexpr int kBatch = 4;    // composited hits whose (L,T) loads are issued together
+constexpr int kBatch = 8;    // composited hits whose (L,T) loads are issued together
 
 // Per-pixel ray direction in LDS, padded to 32 bytes.
 struct __align__(16) RayRec {
