@@ -93,18 +93,19 @@ KERNEL_SOURCES = {
 }
 
 
-def recorded_traffic(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None if absent or if the kernel source changed since it was taken."""
+def recorded_profile(kernel, workload):
+    """The committed rocprofv3 counter record of a kernel (HBM bytes per launch,
+    VALU busy / utilisation), or {} if absent or if the kernel source changed
+    since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f).get(f"{kernel}/{workload}")
     except (OSError, ValueError):
-        return None
+        return {}
     if not rec or rec.get("source_sha256") != source_hash(KERNEL_SOURCES[kernel]):
-        return None
-    return rec.get("hbm_bytes_per_launch")
+        return {}
+    return rec
 
 
 def main():
@@ -263,10 +264,19 @@ def main():
                     frac=round(achieved / peak, 4), f32_flops=w["f32"], f64_flops=w["f64"],
                     hbm_bytes_algorithmic=w["bytes"])
 
+    def with_counters(name):
+        r = roofline(name)
+        rec = recorded_profile("gather" if name == "backward_main" else "forward", args.workload)
+        r["traffic"] = rec.get("hbm_bytes_per_launch")
+        vb = rec.get("valu_busy_pct")
+        r["valu_busy"] = None if vb is None else round(vb / 100.0, 4)
+        vu = rec.get("valu_utilization_pct")
+        r["valu_utilization"] = None if vu is None else round(vu / 100.0, 4)
+        return r
+
     dominant = max(("forward_trace", "backward_main"), key=lambda k: kern_ms[k])
-    roof = roofline(dominant)
+    roof = with_counters(dominant)
     roof["kernel"] = "gather_kernel" if dominant == "backward_main" else "forward_kernel"
-    roof["traffic"] = recorded_traffic("gather" if dominant == "backward_main" else "forward", args.workload)
 
     value = bwd_hits / (call_ms["backward"] * 1e-3)
 
@@ -312,7 +322,7 @@ def main():
         "counters": {name: int(c[i]) for i, name in enumerate(
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
              "bwd_active_units", "fwd_drops"])},
-        "kernels_roofline": {k: roofline(k) for k in work},
+        "kernels_roofline": {k: with_counters(k) for k in work},
     }
     s = json.dumps(line)
     print(s, flush=True)
