@@ -370,6 +370,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.rows = at<float>(f->scratch, L.rows);
   A.row_flag = at<uint8_t>(f->scratch, L.row_flag);
   A.pair_count = f->pair_count;
+  A.logits = g->opacity_logits;
   A.log_scales = g->log_scales;
   A.quats = g->quats;
   A.g_means = g_means;

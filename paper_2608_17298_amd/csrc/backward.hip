@@ -580,7 +580,7 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
   const double qv[4] = {w, x, y, z};
 #pragma unroll
   for (int k = 0; k < 4; ++k) gq[k] = float((dq[k] - qv[k] * proj) * inv_qn);
-  const double sig = A.geom[int64_t(kGeomStride) * i + kGeoSigma];
+  const double sig = 1.0 / (1.0 + exp(-double(A.logits[i])));  // as in the bounds kernel
   A.g_logits[i] = float(sig * (1.0 - sig) * double(acc[9]));
 }
 

@@ -131,6 +131,7 @@ struct BackwardArgs {
   int64_t pair_count;
   int32_t rows_per_pair;  // 64-pixel groups per tile (set by the launcher)
   // raw inputs and outputs
+  const float* logits;
   const float* log_scales;
   const float* quats;
   float* g_means;
