@@ -62,6 +62,9 @@ def parse():
     ap.add_argument("--compare-modes", type=int, default=1, help="also time the other backward modes")
     ap.add_argument("--cpu-baseline", type=int, default=1)
     ap.add_argument("--cpu-pixels", type=int, default=0, help="oracle sample size in pixels (0 = whole frame)")
+    ap.add_argument("--train-steps", type=int, default=12,
+                    help="also time this many multi-view training iterations (0 = skip)")
+    ap.add_argument("--train-views", type=int, default=4, help="orbit views of the training loop")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a device copy of this size (HBM counter calibration) and exit")
     ap.add_argument("--out", default=None, help="also write the JSON line to this file")
@@ -292,6 +295,10 @@ def main():
                                grads_per_s=round(int(cm[gart.CNT_BWD_HITS]) / (bms * 1e-3), 1),
                                float_atomics=int(cm[gart.CNT_BWD_ATOMICS]))
 
+    train = None
+    if args.train_steps > 0:
+        train = train_timing(sc, args.train_steps, args.train_views)
+
     cpu = None
     if args.cpu_baseline:
         cpu = cpu_baseline(sc, dl.cpu().numpy(), args.cpu_pixels)
@@ -323,12 +330,56 @@ def main():
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
              "bwd_active_units", "fwd_drops"])},
         "kernels_roofline": {k: with_counters(k) for k in work},
+        "train_step": train,
     }
     s = json.dumps(line)
     print(s, flush=True)
     if args.out:
         with open(args.out, "w") as f:
             f.write(s + "\n")
+
+
+def train_timing(sc, steps, n_views):
+    """Synthetic multi-view training on the same scene: `n_views` orbit
+    cameras, targets rendered (untimed) from the perturbed-means copy, Adam
+    over L1; per-stage HIP-event times over `steps` iterations after two
+    warm-up iterations."""
+    import dataclasses
+    import torch
+    from paper_2608_17298_amd import gart
+    from paper_2608_17298_amd.scenes import orbit_camera
+    from paper_2608_17298_amd.train import Trainer
+    W, H = sc.camera.width, sc.camera.height
+    cams = [orbit_camera(W, H, 360.0 * k / n_views) for k in range(n_views)]
+    pert = dataclasses.replace(sc, means=sc.means_perturbed)
+    gp = gart.Gaussians.from_scene(pert)
+    st = gart.make_settings(sc.tile, "gather")
+    targets, fr = [], None
+    for c in cams:
+        gc = gart.make_camera(c)
+        fr = gart.prepare(gp, gc, st, fr)
+        t = torch.empty((H, W, 3), dtype=torch.float32, device="cuda")
+        gart.gart_forward(gp, gc, st, fr, t)
+        targets.append(t)
+    del fr, gp
+    tr = Trainer(sc, cams, targets)
+    for it in range(2):
+        tr.step(it % n_views)
+    torch.cuda.synchronize()
+    per, losses = [], []
+    for it in range(steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        tr.step(it % n_views, events=ev)
+        per.append(ev)
+        losses.append(tr.loss.clone())
+    torch.cuda.synchronize()
+    names = ["bounds_tile_map", "forward", "l1", "backward", "adam"]
+    stage = {nm: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in per])) for k, nm in enumerate(names)}
+    total = float(np.mean([e[0].elapsed_time(e[5]) for e in per]))
+    return {"views": n_views, "iterations": steps, "ms_per_iteration": round(total, 4),
+            "stage_ms": {k: round(v, 4) for k, v in stage.items()},
+            "l1_loss_first": round(losses[0].item(), 3), "l1_loss_last": round(losses[-1].item(), 3),
+            "adam": "3DGS-style per-group learning rates (paper_2608_17298_amd/train.py)"}
 
 
 def cpu_baseline(sc, dl, npix):

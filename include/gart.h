@@ -268,6 +268,42 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
                           const gart_frame* frame, const float* dL_dimage, float* g_means,
                           float* g_log_scales, float* g_quats, float* g_logits, float* g_sh, void* stream);
 
+/* ---- Training step around the path (multi-view synthetic training) ----
+ * The paper trains with the usual 3DGS recipe; these two calls close the
+ * loop: the L1 photometric loss supplies the backward's upstream gradient
+ * and Adam updates each parameter group from the gradients gart_backward
+ * writes. */
+
+/* Adam hyper-parameters of one parameter group (host struct). */
+typedef struct {
+  float lr;     /* step size, > 0 */
+  float beta1;  /* first-moment decay, in [0, 1) */
+  float beta2;  /* second-moment decay, in [0, 1) */
+  float eps;    /* added to sqrt(v_hat), >= 0 */
+} gart_adam;
+
+/* Number of fp64 partial sums gart_l1_loss_grad needs for n image floats. */
+int64_t gart_l1_partials(int64_t n);
+
+/* L1 loss against a target image: dL_dimage[k] = sign(image[k] - target[k])
+ * (0 where equal) for k < n (n = height*width*3; all device float32 arrays of
+ * n elements, dL_dimage may not alias the inputs).  If loss is non-NULL it
+ * receives sum_k |image[k] - target[k]| (device fp64 scalar), summed in a fixed
+ * order (deterministic) through partial (device fp64[gart_l1_partials(n)],
+ * caller-owned scratch; may be NULL when loss is NULL).  Asynchronous on
+ * stream.  INVALID_ARG for NULL arrays (when n > 0) or n < 0. */
+gart_status gart_l1_loss_grad(const float* image, const float* target, int64_t n, float* dL_dimage, double* loss,
+                              double* partial, void* stream);
+
+/* One Adam step (Kingma and Ba) on n float32 parameters in place, with the
+ * moment buffers m and v (device float32[n], zero before the first step):
+ *   m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2;
+ *   param -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)
+ * with t = step >= 1.  Asynchronous on stream.  INVALID_ARG for NULL arrays
+ * (when n > 0), n < 0, step < 1 or hyper-parameters outside the ranges above. */
+gart_status gart_adam_step(float* param, const float* grad, float* m, float* v, int64_t n, const gart_adam* h,
+                           int64_t step, void* stream);
+
 /* Human-readable name of a status code (static string). */
 const char* gart_status_string(gart_status status);
 

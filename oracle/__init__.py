@@ -12,6 +12,8 @@ Contents:
     gradient (Sec. 3.5), and the intermediate-buffer address (Sec. 4.3).
   * ``tile_lists``: per-tile primitive lists by plain enumeration of every
     (rectangle, tile) overlap (Sec. 4.3, reverse tile mapping).
+  * ``train_ref``: the L1 loss gradient and the Adam step of the training
+    loop around the path (numpy fp64).
 
 Every function that has no independent pin says so in its docstring.
 """

@@ -142,6 +142,41 @@ int tiles_along(int pixels, int tile) { return (pixels + tile - 1) / tile; }
 
 extern "C" {
 
+int64_t gart_l1_partials(int64_t n) { return n > 0 ? l1_partials(n) : 1; }
+
+gart_status gart_l1_loss_grad(const float* image, const float* target, int64_t n, float* dL_dimage, double* loss,
+                              double* partial, void* stream) {
+  g_err[0] = 0;
+  GART_REQUIRE(n >= 0, "n < 0");
+  GART_REQUIRE(n == 0 || (image && target && dL_dimage), "image/target/dL_dimage is NULL");
+  GART_REQUIRE(loss == nullptr || partial != nullptr, "loss requested without partial scratch");
+  GART_REQUIRE(n == 0 || (dL_dimage != image && dL_dimage != target), "dL_dimage aliases an input");
+  GART_HIP(launch_l1_grad(image, target, n, dL_dimage, partial, loss, static_cast<hipStream_t>(stream)));
+  return GART_OK;
+}
+
+gart_status gart_adam_step(float* param, const float* grad, float* m, float* v, int64_t n, const gart_adam* h,
+                           int64_t step, void* stream) {
+  g_err[0] = 0;
+  GART_REQUIRE(h != nullptr, "hyper-parameters are NULL");
+  GART_REQUIRE(n >= 0 && step >= 1, "n < 0 or step < 1");
+  GART_REQUIRE(n == 0 || (param && grad && m && v), "param/grad/m/v is NULL");
+  GART_REQUIRE(std::isfinite(h->lr) && h->lr > 0.0f, "lr must be > 0");
+  GART_REQUIRE(h->beta1 >= 0.0f && h->beta1 < 1.0f && h->beta2 >= 0.0f && h->beta2 < 1.0f, "betas outside [0, 1)");
+  GART_REQUIRE(std::isfinite(h->eps) && h->eps >= 0.0f, "eps must be >= 0");
+  AdamArgs a;
+  a.lr = h->lr;
+  a.b1 = h->beta1;
+  a.b2 = h->beta2;
+  a.eps = h->eps;
+  a.one_minus_b1 = float(1.0 - double(h->beta1));
+  a.one_minus_b2 = float(1.0 - double(h->beta2));
+  a.inv_c1 = float(1.0 / (1.0 - std::pow(double(h->beta1), double(step))));
+  a.inv_c2 = float(1.0 / (1.0 - std::pow(double(h->beta2), double(step))));
+  GART_HIP(launch_adam(param, grad, m, v, n, a, static_cast<hipStream_t>(stream)));
+  return GART_OK;
+}
+
 const char* gart_status_string(gart_status s) {
   switch (s) {
     case GART_OK: return "GART_OK";

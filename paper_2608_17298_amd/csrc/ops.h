@@ -144,4 +144,20 @@ struct BackwardArgs {
 };
 hipError_t launch_backward(const BackwardArgs& a, hipStream_t s);
 
+// ---- train.hip -----------------------------------------------------------
+constexpr int kL1Block = 256;
+constexpr int kL1Items = 4096;  // image floats per block (and per loss partial)
+int64_t l1_partials(int64_t n);
+// dl = sign(image - target); if loss != NULL, *loss = sum |image - target|
+// (fp64, deterministic) using partial[l1_partials(n)]
+hipError_t launch_l1_grad(const float* image, const float* target, int64_t n, float* dl, double* partial,
+                          double* loss, hipStream_t s);
+
+struct AdamArgs {
+  float lr, b1, b2, eps;
+  float one_minus_b1, one_minus_b2;
+  float inv_c1, inv_c2;  // 1 / (1 - b1^t), 1 / (1 - b2^t)
+};
+hipError_t launch_adam(float* p, const float* g, float* m, float* v, int64_t n, const AdamArgs& h, hipStream_t s);
+
 }  // namespace gart

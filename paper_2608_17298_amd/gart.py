@@ -107,6 +107,12 @@ def lib():
         L.gart_status_string.argtypes = [ctypes.c_int]
         L.gart_last_error.restype = ctypes.c_char_p
         L.gart_last_error.argtypes = []
+        L.gart_l1_partials.restype = ctypes.c_int64
+        L.gart_l1_partials.argtypes = [ctypes.c_int64]
+        L.gart_l1_loss_grad.restype = ctypes.c_int
+        L.gart_l1_loss_grad.argtypes = [_P, _P, ctypes.c_int64, _P, _P, _P, _P]
+        L.gart_adam_step.restype = ctypes.c_int
+        L.gart_adam_step.argtypes = [_P, _P, _P, _P, ctypes.c_int64, _P, ctypes.c_int64, _P]
         _lib = L
     return _lib
 
@@ -350,6 +356,37 @@ def gart_backward(g: Gaussians, camera: gart_camera, settings: gart_settings, fr
                                _ptr(dl_dimage), _ptr(grads["means"]), _ptr(grads["log_scales"]),
                                _ptr(grads["quats"]), _ptr(grads["logits"]), _ptr(grads["sh"]),
                                _stream(stream)), "gart_backward")
+
+
+class gart_adam(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float)]
+
+
+def gart_l1_partials(n: int) -> int:
+    return int(lib().gart_l1_partials(int(n)))
+
+
+def gart_l1_loss_grad(image: torch.Tensor, target: torch.Tensor, dl_dimage: torch.Tensor,
+                      loss: torch.Tensor | None = None, partial: torch.Tensor | None = None, stream=None):
+    """dl_dimage = sign(image - target); loss (device fp64 [1]) = sum |image - target|."""
+    for t in (image, target, dl_dimage):
+        if t.dtype != torch.float32 or t.shape != image.shape:
+            raise ValueError("image, target and dl_dimage must be float32 of one shape")
+    if loss is not None and (loss.dtype != torch.float64 or partial is None or partial.dtype != torch.float64
+                             or partial.numel() < gart_l1_partials(image.numel())):
+        raise ValueError("loss needs a float64 scalar and float64 partials of gart_l1_partials(n)")
+    _check(lib().gart_l1_loss_grad(_ptr(image), _ptr(target), image.numel(), _ptr(dl_dimage), _ptr(loss),
+                                   _ptr(partial), _stream(stream)), "gart_l1_loss_grad")
+
+
+def gart_adam_step(param: torch.Tensor, grad: torch.Tensor, m: torch.Tensor, v: torch.Tensor, h: gart_adam,
+                   step: int, stream=None):
+    """One Adam step in place on a float32 parameter tensor (m and v are its moment buffers)."""
+    for t in (param, grad, m, v):
+        if t.dtype != torch.float32 or t.shape != param.shape:
+            raise ValueError("param, grad, m and v must be float32 of one shape")
+    _check(lib().gart_adam_step(_ptr(param), _ptr(grad), _ptr(m), _ptr(v), param.numel(), ctypes.byref(h),
+                                int(step), _stream(stream)), "gart_adam_step")
 
 
 def empty_grads(g: Gaussians) -> dict:

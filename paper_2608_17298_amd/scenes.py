@@ -105,6 +105,18 @@ def pinhole_camera(width: int, height: int, fov_y_deg: float = 60.0,
                   t=np.array([0.0, 0.0, distance], dtype=np.float32))
 
 
+def orbit_camera(width: int, height: int, azimuth_deg: float, fov_y_deg: float = 60.0,
+                 distance: float = 4.0) -> Camera:
+    """The pinhole camera above, rotated about the world y axis through the
+    origin by azimuth_deg: centre Ry(az) (0, 0, -distance), still looking at
+    the origin (R = Ry(az)^T, t = (0, 0, distance))."""
+    base = pinhole_camera(width, height, fov_y_deg, distance)
+    a = math.radians(azimuth_deg)
+    ry = np.array([[math.cos(a), 0.0, math.sin(a)], [0.0, 1.0, 0.0], [-math.sin(a), 0.0, math.cos(a)]])
+    base.R = ry.T.astype(np.float32)
+    return base
+
+
 def _uniform_ball(rng, n, radius):
     v = rng.standard_normal((n, 3))
     v /= np.linalg.norm(v, axis=1, keepdims=True)
