@@ -43,6 +43,9 @@ GEOM_BYTES = 128 + 16 + 8 + 4  # per staged pair in the forward: fp64 geometry r
 UNIT_BYTES = 104 + 8 + 16 + 8 + 8  # per gather unit: W and o_g, sigma, rect, O_prim, pair offset
 
 
+ALL_MODES = ("gather", "gather_atomic", "scatter", "hybrid")
+
+
 def f32_per_hit_bwd(K):
     # colour 6K, per-hit gradient terms ~25, AW products (9 + 3K), AW accumulations (10 + 3K)
     return 6 * K + 25 + (9 + 3 * K) + (10 + 3 * K)
@@ -58,7 +61,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="1m", choices=["tiny", "small", "1m", "4m", "stress"])
-    ap.add_argument("--mode", default="gather", choices=["gather", "gather_atomic", "scatter"])
+    ap.add_argument("--mode", default="gather", choices=["gather", "gather_atomic", "scatter", "hybrid"])
     ap.add_argument("--compare-modes", type=int, default=1, help="also time the other backward modes")
     ap.add_argument("--cpu-baseline", type=int, default=1)
     ap.add_argument("--cpu-pixels", type=int, default=0, help="oracle sample size in pixels (0 = whole frame)")
@@ -149,7 +152,9 @@ def main():
     gart.gart_forward(gp, cam, st, fp, target)
     del fp
 
-    frame = gart.prepare(g, cam, st, slack=1.05)
+    # 16-byte intermediate entries, so that every backward mode can render
+    # into this frame (the hybrid forward uses the first 4 bytes of each)
+    frame = gart.prepare(g, cam, gart.make_settings(sc.tile, "gather"), slack=1.05)
     image = torch.empty((H, W, 3), dtype=torch.float32, device="cuda")
     gart.gart_forward(g, cam, st, frame, image)
     dl = torch.sign(image - target).contiguous()
@@ -158,7 +163,7 @@ def main():
     # Counting run (device counters; not timed).
     frame.counters = torch.zeros(gart.NUM_COUNTERS, dtype=torch.int64, device="cuda")
     counts = {}
-    for mode in (["gather", "gather_atomic", "scatter"] if args.compare_modes else [args.mode]):
+    for mode in (ALL_MODES if args.compare_modes else [args.mode]):
         frame.counters.zero_()
         stm = gart.make_settings(sc.tile, mode)
         gart.gart_bounds(g, cam, stm, frame)
@@ -285,15 +290,20 @@ def main():
 
     modes = {}
     if args.compare_modes:
-        for mode in ("gather", "gather_atomic", "scatter"):
+        for mode in ALL_MODES:
             stm = gart.make_settings(sc.tile, mode)
+            # render once with this mode's intermediate-buffer format (the
+            # hybrid forward writes T only), then time the backward alone
+            gart.gart_forward(g, cam, stm, frame, image)
             per_m = run_steps(stm, max(5, args.steps // 2), 2, backward_only=True)
             bms = float(np.mean([ms(cl[3], cl[4]) for cl, kr in per_m]))
             kms = float(np.mean([ms(kr[4], kr[5]) for cl, kr in per_m]))
             cm = counts[mode]
             modes[mode] = dict(backward_ms=round(bms, 4), main_kernel_ms=round(kms, 4),
                                grads_per_s=round(int(cm[gart.CNT_BWD_HITS]) / (bms * 1e-3), 1),
-                               float_atomics=int(cm[gart.CNT_BWD_ATOMICS]))
+                               float_atomics=int(cm[gart.CNT_BWD_ATOMICS]),
+                               lt_bytes=int(frame.lt_entries) * (4 if mode == "hybrid" else 16))
+        gart.gart_forward(g, cam, st, frame, image)
 
     train = None
     if args.train_steps > 0:
@@ -328,7 +338,7 @@ def main():
         "forward_rescans": int(c[gart.CNT_FWD_RESCANS]),
         "counters": {name: int(c[i]) for i, name in enumerate(
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
-             "bwd_active_units", "fwd_drops"])},
+             "bwd_active_units", "fwd_drops", "bwd_hybrid_steps"])},
         "kernels_roofline": {k: with_counters(k) for k in work},
         "train_step": train,
     }

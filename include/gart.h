@@ -61,8 +61,16 @@ typedef enum {
 typedef enum {
   GART_BACKWARD_GATHER = 0,        /* (tile, prim) pairs -> per-pair rows -> one reduction per primitive */
   GART_BACKWARD_GATHER_ATOMIC = 1, /* (tile, prim) pairs -> one atomic update per pair (Sec. 4.4 as printed) */
-  GART_BACKWARD_SCATTER = 2        /* pixel-centric control: one atomic update per composited hit (Sec. 3.5) */
+  GART_BACKWARD_SCATTER = 2,       /* pixel-centric control: one atomic update per composited hit (Sec. 3.5) */
+  GART_BACKWARD_HYBRID = 3         /* Sec. 4.4 "Hybrid approach": SH sums gathered per pair, the other 10 sums
+                                      scattered per hit from a back-to-front walk; lt holds T only (4 B) */
 } gart_backward_mode;
+
+/* Layout of gart_frame.lt, chosen by gart_forward from settings->backward_mode. */
+typedef enum {
+  GART_LT_FULL = 0,  /* gart_lt_entry (16 bytes): fixed-point L and T */
+  GART_LT_T_ONLY = 1 /* float T (4 bytes) per entry, entry e at ((float*)lt)[e] (hybrid backward) */
+} gart_lt_format;
 
 /* Pinhole camera.  Host struct, passed by pointer. */
 typedef struct {
@@ -132,8 +140,10 @@ typedef struct {
   uint32_t* pair_prim;    /* [pair_capacity] Gaussian index of each pair */
   int64_t* tile_range;    /* [n_tiles+1] pairs of tile t are [tile_range[t], tile_range[t+1]) */
   /* written by gart_forward, read by gart_backward */
-  int64_t lt_capacity;    /* number of (L,T) entries allocated */
-  gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit */
+  int64_t lt_capacity;    /* number of intermediate entries allocated, each of the size gart_forward
+                             writes for settings->backward_mode (16 bytes; 4 with HYBRID) */
+  gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit; with the hybrid
+                             backward, float[lt_capacity] T only (see gart_lt_format) */
   gart_pixel_state* pixel_state; /* [height*width] per-pixel end marker (see gart_pixel_state) */
   uint32_t* hit_list;     /* [pair_capacity * tile^2] composited hits of each pixel, front to back:
                              for tile t with pairs [b, e) (tile_range), the k-th composited hit of
@@ -157,6 +167,7 @@ typedef struct {
   double color_step;      /* colour per fixed-point unit of lt and pixel_state (see gart_lt_entry):
                              a bound on every Gaussian's colour, divided by 2^32 */
   int32_t stage;          /* 0 none, 1 bounds, 2 tile map, 3 forward */
+  int32_t lt_format;      /* gart_lt_format written by the last gart_forward */
 } gart_frame;
 
 enum {
@@ -169,6 +180,8 @@ enum {
   GART_CNT_BWD_PAIRS = 6,     /* (tile, prim) pairs visited by the backward */
   GART_CNT_BWD_ACTIVE = 7,    /* (pair, 64-pixel group) units with a composited hit (gather) */
   GART_CNT_FWD_DROPS = 8,     /* forward hits dropped from a full hit buffer (found again by a rescan) */
+  GART_CNT_BWD_STEPS = 9,     /* hits walked by the hybrid pixel pass (composited hits, once per window
+                                 of list positions that the tile needs) */
   GART_NUM_COUNTERS = 16
 };
 
@@ -234,7 +247,10 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
  * transmittance in front of the hit, L in the frame's fixed point -- with idx(i,t,p) = O_prim(i) +
  * O_tile(i,t) + O_pixel(i,t,p) (Eq. 16): tiles of the rectangle in
  * row-major order, pixels row-major inside each tile.  Entries for
- * pixels that are not composited hits are left untouched.  hit_list
+ * pixels that are not composited hits are left untouched.  With
+ * settings->backward_mode == HYBRID only T is written (float per entry,
+ * frame->lt_format = GART_LT_T_ONLY, 4 bytes per entry suffice); otherwise
+ * frame->lt_format = GART_LT_FULL (16 bytes per entry).  hit_list
  * records the pair of every composited hit per pixel (entries past a
  * pixel's n_hits are left untouched), so that the gather backward reads
  * which hits to visit instead of re-testing rays.
@@ -260,8 +276,15 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
  *     per-Gaussian accumulators with one atomic update per value.
  *   SCATTER: the pixel-centric control (Sec. 3.5): one lane per pixel, one
  *     atomic add per gradient value per composited hit.
- * The colour in front of and behind each hit comes from the frame's lt and
- * pixel_state (the forward's image is not read); dL_dimage is
+ *   HYBRID (Sec. 4.4, hybrid approach): the SH sums (3K) are gathered per
+ *     unit into rows as in GATHER; a second kernel walks each pixel's
+ *     composited hits back to front (hit_list), forms the colour behind
+ *     each hit from that walk and adds the other 10 terms into per-tile LDS
+ *     accumulators (LDS atomics, so the summation order varies from run to
+ *     run), written into the same rows.  Needs a frame rendered with the same mode (lt_format
+ *     GART_LT_T_ONLY); the other modes need GART_LT_FULL (else INVALID_ARG).
+ * Except in HYBRID, the colour in front of and behind each hit comes from
+ * the frame's lt and pixel_state (the forward's image is not read); dL_dimage is
  * [height,width,3] float32.  Requires gart_forward first (else
  * INVALID_ARG). */
 gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,

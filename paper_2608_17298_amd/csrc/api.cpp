@@ -64,10 +64,11 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
   L.totals = take(64);
   L.partials = take(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
   const size_t AS = size_t(acc_stride(K));
-  L.acc = take(mode == GART_BACKWARD_GATHER ? 4 : size_t(nn) * AS * 4);
+  const bool rows = mode == GART_BACKWARD_GATHER || mode == GART_BACKWARD_HYBRID;
+  L.acc = take(rows ? 4 : size_t(nn) * AS * 4);
   const size_t rpp = size_t(tile) * size_t(tile) / 64;  // partial rows per pair (64-pixel groups)
-  L.rows = take(mode == GART_BACKWARD_GATHER ? size_t(pc) * rpp * AS * 4 : 4);
-  L.row_flag = take(mode == GART_BACKWARD_GATHER ? size_t(pc) * rpp : 4);
+  L.rows = take(rows ? size_t(pc) * rpp * AS * 4 : 4);
+  L.row_flag = take(rows ? size_t(pc) * rpp : 4);
   L.total = off;
   return L;
 }
@@ -95,7 +96,7 @@ gart_status check_settings(const gart_settings* s) {
   GART_REQUIRE(s->alpha_min > 0.0f && s->alpha_min < 1.0f, "alpha_min must be in (0,1)");
   GART_REQUIRE(s->t_min > 0.0f && s->t_min < 1.0f, "t_min must be in (0,1)");
   GART_REQUIRE(s->tile == 8 || s->tile == 16, "tile must be 8 or 16");
-  GART_REQUIRE(s->backward_mode >= 0 && s->backward_mode <= 2, "unknown backward_mode %d", s->backward_mode);
+  GART_REQUIRE(s->backward_mode >= 0 && s->backward_mode <= 3, "unknown backward_mode %d", s->backward_mode);
   return GART_OK;
 }
 
@@ -348,6 +349,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.lt_offset = f->lt_offset;
   A.sh = g->sh;
   A.lt = reinterpret_cast<uint4*>(f->lt);
+  A.lt_t_only = settings->backward_mode == GART_BACKWARD_HYBRID;
   A.inv_color_step = 1.0 / f->color_step;
   A.image = image;
   A.pixel_state = f->pixel_state;
@@ -356,6 +358,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
   GART_HIP(launch_forward(A, s));
+  f->lt_format = A.lt_t_only ? GART_LT_T_ONLY : GART_LT_FULL;
   f->stage = 3;
   return GART_OK;
 }
@@ -373,6 +376,9 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
+  GART_REQUIRE(f->lt_format == (settings->backward_mode == GART_BACKWARD_HYBRID ? GART_LT_T_ONLY : GART_LT_FULL),
+               "frame lt_format %d does not match backward mode %d (render with the same mode)", f->lt_format,
+               settings->backward_mode);
   if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
   const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode, settings->tile);

@@ -81,6 +81,26 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
     for (int ch = 0; ch < 3; ++ch) acc[10 + 3 * k + ch] = fmaf(dc[ch], Y[k], acc[10 + 3 * k + ch]);
 }
 
+// SH part of one composited hit (hybrid mode): dL/dc = T a g on unclamped
+// channels, dL/dsh_k += dL/dc Y_k; the geometric sums come from the pixel
+// pass.  Same rounding as hit_grad_acc.
+template <int K>
+__device__ __forceinline__ void hit_sh_acc(double D2, double sigma, const float sh[3 * K], const float Y[K],
+                                           const float g[3], float T, float acc[acc_width(K)]) {
+  const float rho = __builtin_amdgcn_exp2f(float(-0.72134752044448170368 * D2));
+  const float a = float(sigma) * rho;
+  const float ta = T * a;
+#pragma unroll
+  for (int ch = 0; ch < 3; ++ch) {
+    float v = 0.5f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) v = fmaf(sh[3 * k + ch], Y[k], v);
+    const float dc = v > 0.0f ? ta * g[ch] : 0.0f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) acc[10 + 3 * k + ch] = fmaf(dc, Y[k], acc[10 + 3 * k + ch]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Gather: one workgroup per tile.  The tile's pixels form G = TILE^2 / 64
 // groups of 64 pixels (whole rows, one wave each); the unit of work is a
@@ -135,8 +155,10 @@ __device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint3
   return kept;
 }
 
-template <int TILE, int K, bool ATOMIC>
+template <int TILE, int K, bool ATOMIC, bool HYBRID>
 __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
+  // HYBRID: the intermediate buffer holds T only (4 bytes per entry) and the
+  // unit accumulates only the SH sums (the pixel pass adds the others).
   constexpr int NT = TILE * TILE;
   constexpr int G = NT / 64;      // pixel groups (waves) per tile
   constexpr int R = 64 / TILE;    // tile rows per group
@@ -280,7 +302,13 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       // offset inside rect cap tile (Eq. 16).
       const int64_t base = A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, xa, ya) +
                            int64_t(oy + g * R - ya) * w + (ox - xa);
-      auto lt_at = [&](int b) { return A.lt[base + int64_t(b / TILE) * w + (b % TILE)]; };
+      auto lt_at = [&](int b) {
+        const int64_t e = base + int64_t(b / TILE) * w + (b % TILE);
+        if constexpr (HYBRID)
+          return make_uint4(0, 0, 0, __float_as_uint(reinterpret_cast<const float*>(A.lt)[e]));
+        else
+          return A.lt[e];
+      };
       float acc[AW];
 #pragma unroll
       for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
@@ -322,7 +350,10 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
           const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[lp][4]);
           const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
           const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
-          hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
+          if constexpr (HYBRID)
+            hit_sh_acc<K>(D2, sigma, sh, Y, gr, __uint_as_float(lv[t].w), acc);
+          else
+            hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
         }
       }
       ++n_active;
@@ -355,6 +386,141 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     count_add(A.counters + GART_CNT_BWD_HITS, n_hits);
     count_add(A.counters + GART_CNT_BWD_ATOMICS, n_atom);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Hybrid pixel pass: each lane (pixel) walks its own composited hits back to
+// front (the forward's hit list), forming the colour behind each hit, S, from
+// the walk in fp64 (the intermediate buffer holds T only, so S cannot come
+// from C - L), and adds the hit's 10 geometric terms (2u x_g, 2u x_g x_g^T,
+// dL/dsigma) into LDS accumulators of its (list position, pixel group) with
+// LDS float atomics.  The tile's list is covered in windows of kWin
+// positions; each window is walked once more (S needs every hit behind), and
+// its touched accumulators are written into the (pair, group) rows that the
+// SH gather filled (zeros there).
+// ---------------------------------------------------------------------------
+template <int TILE>
+struct HybridWindow {
+  static constexpr int G = TILE * TILE / 64;
+  static constexpr int kWin = TILE == 8 ? 384 : 128;  // list positions per window
+};
+
+template <int TILE, int K>
+__global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A) {
+  constexpr int NT = TILE * TILE;
+  constexpr int G = HybridWindow<TILE>::G, kWin = HybridWindow<TILE>::kWin;
+  constexpr int AS = acc_stride(K);
+  __shared__ float s_acc[kWin * G][10];
+  __shared__ uint8_t s_touch[kWin * G];
+  __shared__ int s_maxpos[G];
+
+  const int n_tiles = A.tiles_x * A.tiles_y;
+  const int tile = xcd_tile(blockIdx.x, n_tiles, A.tiles_x);
+  const int tx = tile % A.tiles_x, ty = tile / A.tiles_x;
+  const int tid = threadIdx.x, grp = tid / 64;
+  const int px = tx * TILE + tid % TILE, py = ty * TILE + tid / TILE;
+  const bool valid = px < A.cam.W && py < A.cam.H;
+  double d[3];
+  pixel_ray(A.cam, valid ? px : 0, valid ? py : 0, d);
+  float Y[K];
+  sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
+  float g[3] = {0.0f, 0.0f, 0.0f};
+  int nh = 0;
+  if (valid) {
+    const int64_t p = int64_t(py) * A.cam.W + px;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) g[ch] = A.dl_dimage[3 * p + ch];
+    nh = int(A.pixel_state[p].n_hits);
+  }
+  const int64_t beg = A.tile_range[tile];
+  const uint32_t* hl = A.hit_list + int64_t(NT) * beg + tid;
+  uint32_t n_walk = 0;
+
+  for (int w0 = 0;; w0 += kWin) {
+    for (int u = tid; u < kWin * G; u += NT) {
+#pragma unroll
+      for (int v = 0; v < 10; ++v) s_acc[u][v] = 0.0f;
+      s_touch[u] = 0;
+    }
+    __syncthreads();
+    double S[3] = {0.0, 0.0, 0.0};  // colour behind the current hit
+    int maxpos = -1;
+    for (int k = nh - 1; k >= 0; --k) {
+      const int pos = int(hl[int64_t(NT) * k]);
+      maxpos = max(maxpos, pos);
+      const uint32_t i = A.pair_prim[beg + pos];
+      const double* Gm = A.geom + int64_t(kGeomStride) * i;
+      double W[9], og[3];
+#pragma unroll
+      for (int e = 0; e < 9; ++e) W[e] = Gm[e];
+#pragma unroll
+      for (int e = 0; e < 3; ++e) og[e] = Gm[kGeoOg + e];
+      const double sigma = Gm[kGeoSigma];
+      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
+      const float T = reinterpret_cast<const float*>(A.lt)[A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py)];
+      double D2, xg[3];
+      hit_point(W, og, d, &D2, xg);
+      const float rho = __builtin_amdgcn_exp2f(float(-0.72134752044448170368 * D2));
+      const float a = float(sigma) * rho;
+      const float* shp = A.sh + int64_t(i) * (3 * K);
+      float c[3];
+#pragma unroll
+      for (int ch = 0; ch < 3; ++ch) {
+        float cv = 0.5f;
+#pragma unroll
+        for (int kk = 0; kk < K; ++kk) cv = fmaf(shp[3 * kk + ch], Y[kk], cv);
+        c[ch] = cv > 0.0f ? cv : 0.0f;
+      }
+      if (pos >= w0 && pos < w0 + kWin) {
+        const float inv = __builtin_amdgcn_rcpf(1.0f - a);
+        float dlda = 0.0f;
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) dlda = fmaf(g[ch], fmaf(T, c[ch], -float(S[ch]) * inv), dlda);
+        const float u2 = -a * dlda;
+        const float x = float(xg[0]), y = float(xg[1]), z = float(xg[2]);
+        const float ux = u2 * x, uy = u2 * y, uz = u2 * z;
+        float* acc = s_acc[(pos - w0) * G + grp];
+        atomicAdd(acc + 0, ux);
+        atomicAdd(acc + 1, uy);
+        atomicAdd(acc + 2, uz);
+        atomicAdd(acc + 3, ux * x);
+        atomicAdd(acc + 4, uy * y);
+        atomicAdd(acc + 5, uz * z);
+        atomicAdd(acc + 6, ux * y);
+        atomicAdd(acc + 7, ux * z);
+        atomicAdd(acc + 8, uy * z);
+        atomicAdd(acc + 9, dlda * rho);
+        s_touch[(pos - w0) * G + grp] = 1;
+      }
+      const double wt = double(T) * double(a);
+#pragma unroll
+      for (int ch = 0; ch < 3; ++ch) S[ch] = fma(wt, double(c[ch]), S[ch]);
+      ++n_walk;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) maxpos = max(maxpos, __shfl_xor(maxpos, off));
+    if (tid % 64 == 0) s_maxpos[grp] = maxpos;
+    __syncthreads();
+    // write the window's touched accumulators into their rows
+    for (int u = tid; u < kWin * G; u += NT) {
+      if (!s_touch[u]) continue;
+      const uint32_t i = A.pair_prim[beg + w0 + u / G];
+      const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
+      const int tx0 = r.x / TILE, ty0 = r.y / TILE, tx1 = r.z / TILE;
+      const int64_t row = (A.pair_offset[i] + int64_t(ty - ty0) * (tx1 - tx0 + 1) + (tx - tx0)) * G + u % G;
+      float4* dst = reinterpret_cast<float4*>(A.rows + row * AS);
+      const float* v = s_acc[u];
+      dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+      dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+      reinterpret_cast<float2*>(dst + 2)[0] = make_float2(v[8], v[9]);
+    }
+    int mp = s_maxpos[0];
+#pragma unroll
+    for (int w = 1; w < G; ++w) mp = max(mp, s_maxpos[w]);
+    if (mp < w0 + kWin) break;
+    __syncthreads();  // the window's LDS arrays are cleared by the next window
+  }
+  if (A.counters) count_add(A.counters + GART_CNT_BWD_STEPS, n_walk);
 }
 
 // ---------------------------------------------------------------------------
@@ -591,17 +757,23 @@ hipError_t launch_tk(const BackwardArgs& args, hipStream_t s) {
   a.rows_per_pair = TILE * TILE / 64;
   const int n_tiles = a.tiles_x * a.tiles_y;
   hipError_t e = hipSuccess;
-  const bool rows = a.mode == GART_BACKWARD_GATHER;
-  e = rows ? fill_u8(a.row_flag, 0, a.pair_count * a.rows_per_pair, s) : fill_f32(a.acc, 0.0f, a.n * AS, s);
-  if (e != hipSuccess) return e;
+  const bool hybrid = a.mode == GART_BACKWARD_HYBRID;
+  const bool rows = a.mode == GART_BACKWARD_GATHER || hybrid;
+  if (rows && (e = fill_u8(a.row_flag, 0, a.pair_count * a.rows_per_pair, s)) != hipSuccess) return e;
+  if (!rows && (e = fill_f32(a.acc, 0.0f, a.n * AS, s)) != hipSuccess) return e;
   if ((e = record(a.ev[0], s)) != hipSuccess) return e;
   if (n_tiles > 0) {
-    if (rows)
-      gather_kernel<TILE, K, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
-    else if (a.mode == GART_BACKWARD_GATHER_ATOMIC)
-      gather_kernel<TILE, K, true><<<n_tiles, TILE * TILE, 0, s>>>(a);
-    else
+    if (a.mode == GART_BACKWARD_GATHER) {
+      gather_kernel<TILE, K, false, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
+    } else if (a.mode == GART_BACKWARD_GATHER_ATOMIC) {
+      gather_kernel<TILE, K, true, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
+    } else if (hybrid) {
+      gather_kernel<TILE, K, false, true><<<n_tiles, TILE * TILE, 0, s>>>(a);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      hybrid_pixel_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
+    } else {
       scatter_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = record(a.ev[1], s)) != hipSuccess) return e;

@@ -35,7 +35,7 @@ constexpr int kMaxPasses = 1 << 20;
 // row: [0..8] W, [9..11] o_g, [12] D2c, [13] sigma, [14] depth key,
 // [15] O_prim (int64 bits), [16..17] rect (4 x int32), [18] index (uint32)
 
-template <int TILE, int K>
+template <int TILE, int K, bool T_ONLY>
 __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int NT = TILE * TILE;
   constexpr int KB = GART_FWD_KB;  // per-lane hit buffer (registers)
@@ -122,8 +122,11 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     // k-th composited hit of this pixel -> its list position (read by the
     // gather backward)
     A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = bc[0];
-    A.lt[lt_base + bi[0]] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
-                                       color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
+    if constexpr (T_ONLY)
+      reinterpret_cast<float*>(A.lt)[lt_base + bi[0]] = float(T);
+    else
+      A.lt[lt_base + bi[0]] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
+                                         color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
     const double w = T * a;
     L0 = fma(w, double(c[0]), L0);
     L1 = fma(w, double(c[1]), L1);
@@ -303,7 +306,10 @@ hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
   const int n_tiles = a.tiles_x * a.tiles_y;
   hipError_t e = record(a.ev_begin, s);
   if (e != hipSuccess) return e;
-  forward_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
+  if (a.lt_t_only)
+    forward_kernel<TILE, K, true><<<n_tiles, TILE * TILE, 0, s>>>(a);
+  else
+    forward_kernel<TILE, K, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(a.ev_end, s);
 }

@@ -32,11 +32,14 @@ GART_ERR_UNSUPPORTED = -4
 GATHER = 0
 GATHER_ATOMIC = 1
 SCATTER = 2
-MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER}
+HYBRID = 3
+MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER, "hybrid": HYBRID}
+LT_FULL, LT_T_ONLY = 0, 1
 
 CNT_FWD_HITS, CNT_FWD_TESTS, CNT_FWD_RESCANS = 0, 1, 2
 CNT_BWD_HITS, CNT_BWD_TESTS, CNT_BWD_ATOMICS, CNT_BWD_PAIRS, CNT_BWD_ACTIVE = 3, 4, 5, 6, 7
 CNT_FWD_DROPS = 8
+CNT_BWD_STEPS = 9
 NUM_COUNTERS = 16
 EV_SORT, EV_FWD, EV_BWD, EV_REDUCE = 0, 2, 4, 6  # begin index; end = begin + 1
 NUM_EVENTS = 8
@@ -67,7 +70,8 @@ class gart_frame(ctypes.Structure):
                 ("scratch", _P), ("scratch_bytes", ctypes.c_size_t), ("counters", _P),
                 ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
-                ("color_step", ctypes.c_double), ("stage", ctypes.c_int32)]
+                ("color_step", ctypes.c_double), ("stage", ctypes.c_int32),
+                ("lt_format", ctypes.c_int32)]
 
 
 class GartError(RuntimeError):
@@ -235,8 +239,10 @@ class Frame:
         self._alloc_pairs(pair_capacity)
 
     def _alloc_lt(self, cap):
-        # gart_lt_entry: three fixed-point colour words and the float bits of T
-        self.lt = torch.empty((max(int(cap), 1), 4), dtype=torch.int32, device=self.device)
+        # gart_lt_entry: three fixed-point colour words and the float bits of
+        # T; the hybrid backward's forward writes T only (one word)
+        words = 1 if self.settings.backward_mode == HYBRID else 4
+        self.lt = torch.empty((max(int(cap), 1), words), dtype=torch.int32, device=self.device)
         self.lt_capacity = int(cap)
 
     def _alloc_pairs(self, cap):
@@ -248,7 +254,7 @@ class Frame:
         self.pair_capacity = cap
         # sized for every backward mode, so one frame serves all of them
         nbytes = 0
-        for mode in (GATHER, GATHER_ATOMIC, SCATTER):
+        for mode in (GATHER, GATHER_ATOMIC, SCATTER, HYBRID):
             st = gart_settings(self.settings.alpha_min, self.settings.t_min, self.settings.tile, mode)
             nbytes = max(nbytes, gart_scratch_bytes(self.n, self.sh_degree, cap, self.camera, st))
         self.scratch = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
@@ -291,8 +297,11 @@ class Frame:
         return float(self.c.color_step)
 
     def lt_entries_host(self, index: torch.Tensor):
-        """(L [m,3] float64, T [m] float32) of the listed (L,T) entries, on the host."""
+        """(L [m,3] float64, T [m] float32) of the listed (L,T) entries, on
+        the host; L is None for a T-only buffer (hybrid backward)."""
         raw = self.lt[index].cpu().numpy()
+        if int(self.c.lt_format) == LT_T_ONLY:
+            return None, raw[:, 0].copy().view(np.float32)
         L = raw[:, :3].view(np.uint32).astype(np.float64) * self.color_step
         return L, raw[:, 3].copy().view(np.float32)
 
@@ -338,6 +347,10 @@ def gart_forward(g: Gaussians, camera: gart_camera, settings: gart_settings, fra
     """Forward trace (Sec. 3.2-3.3, 4.3); image is [H,W,3] float32."""
     if image.dtype != torch.float32 or image.shape != (camera.height, camera.width, 3):
         raise ValueError("image must be float32 [H,W,3]")
+    if settings.backward_mode != HYBRID and frame.lt.shape[1] != 4:
+        # lt_capacity counts entries of the format this call writes
+        raise ValueError("frame's intermediate buffer holds T only (allocated for the hybrid backward); "
+                         "a 16-byte-entry render needs a frame allocated for another mode")
     gs = g.c_struct()
     fs = frame.c_struct()
     _check(lib().gart_forward(ctypes.byref(gs), ctypes.byref(camera), ctypes.byref(settings), ctypes.byref(fs),

@@ -130,13 +130,66 @@ def test_forward_lt_entries(name):
     assert np.abs(T.astype(np.float64) - LT[:, 3]).max() <= 1e-6
 
 
-@pytest.mark.parametrize("mode", ["gather", "gather_atomic", "scatter"])
+@pytest.mark.parametrize("mode", ["gather", "gather_atomic", "scatter", "hybrid"])
 @pytest.mark.parametrize("name", SCENES)
 def test_backward_parity(name, mode):
     sc, o, info, ren, grads, gpu = _case(name, mode)
     for k in GROUPS:
         e = rel_l2(gpu["grads"][k], grads[k])
         assert e <= GRAD_TOL, (k, e)
+
+
+@pytest.mark.parametrize("name", ["tiny", "1m_reduced", "random_sh3"])
+def test_hybrid_t_only_buffer(name):
+    """Hybrid mode: the forward writes only T per entry (4 bytes, Sec. 4.4
+    hybrid approach) at the same idx(i,t,p), the image is the gather mode's
+    bit for bit, the pixel pass walks every composited hit (once per window
+    of list positions), no global atomics are issued, and repeated runs
+    agree to float rounding (LDS atomics vary the summation order)."""
+    import torch
+    from paper_2608_17298_amd import gart
+    sc, o, info, ren, grads, gpu = _case(name, "hybrid")
+    ref = _case(name, "gather")[5]
+    assert np.array_equal(gpu["image"], ref["image"])
+    assert np.array_equal(gpu["n_hits"], ref["n_hits"])
+    c = gpu["counters"]
+    assert c[gart.CNT_BWD_ATOMICS] == 0
+    assert c[gart.CNT_BWD_HITS] == c[gart.CNT_FWD_HITS]
+    assert c[gart.CNT_BWD_ACTIVE] == ref["counters"][gart.CNT_BWD_ACTIVE]
+    assert c[gart.CNT_BWD_STEPS] >= c[gart.CNT_BWD_HITS]
+    if np.diff(gpu["tile_range"]).max() <= (384 if sc.tile == 8 else 128):  # one window per tile
+        assert c[gart.CNT_BWD_STEPS] == c[gart.CNT_BWD_HITS]
+    h = run_gpu(sc, mode="hybrid", keep_frame=True)
+    for k in GROUPS:
+        assert rel_l2(h["grads"][k], gpu["grads"][k]) <= 1e-6, k
+    fr = h["frame"]
+    assert fr.lt.shape[1] == 1 and int(fr.c.lt_format) == gart.LT_T_ONLY
+    ok = np.nonzero(ren["margin"] >= AMBIG)[0]
+    pix = ok[ren["n_included"][ok] > 0][:20000]
+    off, prim, LT, tau = o.records(pix, ren["n_included"][pix])
+    idx = o.lt_index(sc.tile, prim, np.repeat(pix, np.diff(off)))
+    L, T = fr.lt_entries_host(torch.from_numpy(idx).cuda())
+    assert L is None
+    assert np.abs(T.astype(np.float64) - LT[:, 3]).max() <= 1e-6
+
+
+def test_backward_rejects_other_lt_format():
+    """A frame rendered for one lt format cannot feed a backward that reads
+    the other (INVALID_ARG, nothing launched)."""
+    import torch
+    from paper_2608_17298_amd import gart
+    sc = make_scene("tiny")
+    cam = gart.make_camera(sc.camera)
+    g = gart.Gaussians.from_scene(sc)
+    dl = torch.from_numpy(np.ascontiguousarray(sc.dl_dimage, dtype=np.float32)).cuda()
+    for fwd, bwd in [("gather", "hybrid"), ("hybrid", "gather"), ("hybrid", "scatter")]:
+        st = gart.make_settings(sc.tile, fwd)
+        frame = gart.prepare(g, cam, st)
+        image = torch.empty((cam.height, cam.width, 3), dtype=torch.float32, device="cuda")
+        gart.gart_forward(g, cam, st, frame, image)
+        with pytest.raises(gart.GartError, match="lt_format"):
+            gart.gart_backward(g, cam, gart.make_settings(sc.tile, bwd), frame, dl, gart.empty_grads(g))
+    torch.cuda.synchronize()
 
 
 def test_gather_deterministic():

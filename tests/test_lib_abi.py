@@ -92,3 +92,35 @@ def test_scratch_bytes_monotone(lib):
     assert 0 < a < b < c
     st.backward_mode = 1
     assert gart.gart_scratch_bytes(1000, 3, 100_000, cam, st) < b  # no per-pair rows needed
+    st.backward_mode = 3
+    assert gart.gart_scratch_bytes(1000, 3, 100_000, cam, st) == b  # the same per-pair rows
+
+
+def test_ctypes_structs_match_header(tmp_path):
+    """Every field of the ctypes mirrors sits at the offset the C compiler
+    gives it from include/gart.h (and the struct sizes agree), so the
+    binding passes the layout the library reads."""
+    import subprocess
+    from paper_2608_17298_amd import gart
+    structs = [gart.gart_camera, gart.gart_gaussians, gart.gart_settings, gart.gart_frame, gart.gart_adam]
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "gart.h"', "int main(void) {"]
+    for s in structs:
+        lines.append(f'  printf("{s.__name__} size %zu\\n", sizeof({s.__name__}));')
+        for f in s._fields_:
+            lines.append(f'  printf("{s.__name__} {f[0]} %zu\\n", offsetof({s.__name__}, {f[0]}));')
+    lines.append('  printf("gart_pixel_state size %zu\\n", sizeof(gart_pixel_state));')
+    lines.append('  printf("gart_lt_entry size %zu\\n", sizeof(gart_lt_entry));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = {}
+    for ln in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.splitlines():
+        a, b, c = ln.split()
+        got[(a, b)] = int(c)
+    for s in structs:
+        assert got[(s.__name__, "size")] == ctypes.sizeof(s), s.__name__
+        for f in s._fields_:
+            assert got[(s.__name__, f[0])] == getattr(s, f[0]).offset, (s.__name__, f[0])
+    assert got[("gart_pixel_state", "size")] == 32 and got[("gart_lt_entry", "size")] == 16
