@@ -396,7 +396,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
 // dL/dsigma) into LDS accumulators of its (list position, pixel group) with
 // LDS float atomics.  The tile's list is covered in windows of kWin
 // positions; each window is walked once more (S needs every hit behind), and
-// its touched accumulators are written into the (pair, group) rows that the
+// its nonzero accumulators are written into the (pair, group) rows that the
 // SH gather filled (zeros there).
 // ---------------------------------------------------------------------------
 template <int TILE>
@@ -411,7 +411,6 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
   constexpr int G = HybridWindow<TILE>::G, kWin = HybridWindow<TILE>::kWin;
   constexpr int AS = acc_stride(K);
   __shared__ float s_acc[kWin * G][10];
-  __shared__ uint8_t s_touch[kWin * G];
   __shared__ int s_maxpos[G];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
@@ -440,7 +439,6 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
     for (int u = tid; u < kWin * G; u += NT) {
 #pragma unroll
       for (int v = 0; v < 10; ++v) s_acc[u][v] = 0.0f;
-      s_touch[u] = 0;
     }
     __syncthreads();
     double S[3] = {0.0, 0.0, 0.0};  // colour behind the current hit
@@ -490,7 +488,6 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
         atomicAdd(acc + 7, ux * z);
         atomicAdd(acc + 8, uy * z);
         atomicAdd(acc + 9, dlda * rho);
-        s_touch[(pos - w0) * G + grp] = 1;
       }
       const double wt = double(T) * double(a);
 #pragma unroll
@@ -501,9 +498,14 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
     for (int off = 32; off > 0; off >>= 1) maxpos = max(maxpos, __shfl_xor(maxpos, off));
     if (tid % 64 == 0) s_maxpos[grp] = maxpos;
     __syncthreads();
-    // write the window's touched accumulators into their rows
+    // write the window's nonzero accumulators into their rows (a unit whose
+    // sums are all zero keeps the zeros the SH gather wrote; a position with
+    // no hit in this group has no row to write and stays zero)
     for (int u = tid; u < kWin * G; u += NT) {
-      if (!s_touch[u]) continue;
+      bool nz = false;
+#pragma unroll
+      for (int v = 0; v < 10; ++v) nz |= s_acc[u][v] != 0.0f;
+      if (!nz) continue;
       const uint32_t i = A.pair_prim[beg + w0 + u / G];
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
       const int tx0 = r.x / TILE, ty0 = r.y / TILE, tx1 = r.z / TILE;
