@@ -44,6 +44,8 @@ UNIT_BYTES = 104 + 8 + 16 + 8 + 8  # per gather unit: W and o_g, sigma, rect, O_
 
 
 ALL_MODES = ("gather", "gather_atomic", "scatter", "hybrid")
+# backward mode + intermediate-buffer precision pairs timed beside the default
+STORAGE_VARIANTS = (("gather", "fixed16"), ("gather", "half"), ("hybrid", "fixed16"))
 
 
 def f32_per_hit_bwd(K):
@@ -302,7 +304,14 @@ def main():
             modes[mode] = dict(backward_ms=round(bms, 4), main_kernel_ms=round(kms, 4),
                                grads_per_s=round(int(cm[gart.CNT_BWD_HITS]) / (bms * 1e-3), 1),
                                float_atomics=int(cm[gart.CNT_BWD_ATOMICS]),
-                               lt_bytes=int(frame.lt_entries) * (4 if mode == "hybrid" else 16))
+                               lt_bytes=int(frame.lt_entries) * gart.gart_lt_entry_bytes(stm))
+        for mode, prec in STORAGE_VARIANTS:
+            stm = gart.make_settings(sc.tile, mode, lt_precision=prec)
+            per_m = run_steps(stm, max(5, args.steps // 2), 2)
+            fms = float(np.mean([ms(cl[2], cl[3]) for cl, kr in per_m]))
+            bms = float(np.mean([ms(cl[3], cl[4]) for cl, kr in per_m]))
+            modes[f"{mode}+{prec}"] = dict(forward_ms=round(fms, 4), backward_ms=round(bms, 4),
+                                           lt_bytes=int(frame.lt_entries) * gart.gart_lt_entry_bytes(stm))
         gart.gart_forward(g, cam, st, frame, image)
 
     train = None

@@ -66,11 +66,26 @@ typedef enum {
                                       scattered per hit from a back-to-front walk; lt holds T only (4 B) */
 } gart_backward_mode;
 
-/* Layout of gart_frame.lt, chosen by gart_forward from settings->backward_mode. */
+/* Layout of gart_frame.lt, chosen by gart_forward from settings->backward_mode
+ * and settings->lt_precision (see gart_lt_entry_bytes). */
 typedef enum {
-  GART_LT_FULL = 0,  /* gart_lt_entry (16 bytes): fixed-point L and T */
-  GART_LT_T_ONLY = 1 /* float T (4 bytes) per entry, entry e at ((float*)lt)[e] (hybrid backward) */
+  GART_LT_FULL = 0,   /* gart_lt_entry (16 bytes): fixed-point L and float T */
+  GART_LT_T_ONLY = 1, /* float T (4 bytes) per entry, entry e at ((float*)lt)[e] (hybrid backward) */
+  GART_LT_HALF = 2,   /* fp16 L.r, L.g, L.b, T (8 bytes, in that order; Sec. 6 fp16 storage) */
+  GART_LT_T_HALF = 3, /* fp16 T (2 bytes) per entry (hybrid backward with fp16 storage) */
+  GART_LT_FIXED16 = 4,/* uint16 L.r, L.g, L.b in units of color_step * 2^16, then uint16 T code
+                         q = round(-log2(T) * 4096), T = 2^(-q / 4096) (8 bytes) */
+  GART_LT_T_LOG16 = 5 /* uint16 T code as in GART_LT_FIXED16 (2 bytes; hybrid backward) */
 } gart_lt_format;
+
+typedef enum {
+  GART_LT_PRECISION_FULL = 0, /* 16-byte (L,T) entries, or 4-byte T with the hybrid backward */
+  GART_LT_PRECISION_HALF = 1, /* fp16 entries: 8 bytes, or 2 bytes with the hybrid backward;
+                                 values are rounded to float, then to the nearest fp16 */
+  GART_LT_PRECISION_FIXED16 = 2 /* 16-bit fixed-point L and log-coded T: 8 bytes, or 2 bytes with
+                                   the hybrid backward; needs t_min >= 2^-15 (T of every composited
+                                   hit is at least t_min, so its code fits 16 bits) */
+} gart_lt_precision;
 
 /* Pinhole camera.  Host struct, passed by pointer. */
 typedef struct {
@@ -97,6 +112,7 @@ typedef struct {
   float t_min;            /* stop a ray once its transmittance drops below this; in (0, 1) */
   int32_t tile;           /* tile edge in pixels: 8 or 16 (Sec. 4.4 uses 8) */
   int32_t backward_mode;  /* gart_backward_mode */
+  int32_t lt_precision;   /* gart_lt_precision */
 } gart_settings;
 
 /* Per-pixel state the forward leaves for the backward (32 bytes): the depth
@@ -140,10 +156,10 @@ typedef struct {
   uint32_t* pair_prim;    /* [pair_capacity] Gaussian index of each pair */
   int64_t* tile_range;    /* [n_tiles+1] pairs of tile t are [tile_range[t], tile_range[t+1]) */
   /* written by gart_forward, read by gart_backward */
-  int64_t lt_capacity;    /* number of intermediate entries allocated, each of the size gart_forward
-                             writes for settings->backward_mode (16 bytes; 4 with HYBRID) */
-  gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit; with the hybrid
-                             backward, float[lt_capacity] T only (see gart_lt_format) */
+  int64_t lt_capacity;    /* number of intermediate entries allocated, each of
+                             gart_lt_entry_bytes(settings) bytes */
+  gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit, in the layout
+                             frame->lt_format names (see gart_lt_format) */
   gart_pixel_state* pixel_state; /* [height*width] per-pixel end marker (see gart_pixel_state) */
   uint32_t* hit_list;     /* [pair_capacity * tile^2] composited hits of each pixel, front to back:
                              for tile t with pairs [b, e) (tile_range), the k-th composited hit of
@@ -196,6 +212,13 @@ enum {
   GART_EV_REDUCE_END = 7,
   GART_NUM_EVENTS = 8
 };
+
+/* Bytes per intermediate-buffer entry that gart_forward writes for these
+ * settings: 16 (GART_LT_FULL), 4 (GART_LT_T_ONLY), 8 (GART_LT_HALF,
+ * GART_LT_FIXED16) or 2 (GART_LT_T_HALF, GART_LT_T_LOG16); 0 for invalid
+ * settings.  lt must hold lt_capacity such
+ * entries (Sec. 4.3 Eq. 15; Sec. 4.4 hybrid approach; Sec. 6 fp16). */
+int32_t gart_lt_entry_bytes(const gart_settings* settings);
 
 /* Bytes of scratch a frame needs for n Gaussians of the given SH degree and
  * pair_capacity pair slots (all backward modes covered).  Pure host

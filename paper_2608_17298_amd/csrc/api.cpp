@@ -97,7 +97,18 @@ gart_status check_settings(const gart_settings* s) {
   GART_REQUIRE(s->t_min > 0.0f && s->t_min < 1.0f, "t_min must be in (0,1)");
   GART_REQUIRE(s->tile == 8 || s->tile == 16, "tile must be 8 or 16");
   GART_REQUIRE(s->backward_mode >= 0 && s->backward_mode <= 3, "unknown backward_mode %d", s->backward_mode);
+  GART_REQUIRE(s->lt_precision >= GART_LT_PRECISION_FULL && s->lt_precision <= GART_LT_PRECISION_FIXED16,
+               "unknown lt_precision %d", s->lt_precision);
+  GART_REQUIRE(s->lt_precision != GART_LT_PRECISION_FIXED16 || s->t_min >= 0x1p-15f,
+               "lt_precision FIXED16 needs t_min >= 2^-15 (T codes are 16 bits)");
   return GART_OK;
+}
+
+int lt_format_for(const gart_settings* s) {
+  const bool hybrid = s->backward_mode == GART_BACKWARD_HYBRID;
+  if (s->lt_precision == GART_LT_PRECISION_HALF) return hybrid ? GART_LT_T_HALF : GART_LT_HALF;
+  if (s->lt_precision == GART_LT_PRECISION_FIXED16) return hybrid ? GART_LT_T_LOG16 : GART_LT_FIXED16;
+  return hybrid ? GART_LT_T_ONLY : GART_LT_FULL;
 }
 
 gart_status check_gaussians(const gart_gaussians* g) {
@@ -190,6 +201,13 @@ const char* gart_status_string(gart_status s) {
 }
 
 const char* gart_last_error(void) { return g_err; }
+
+int32_t gart_lt_entry_bytes(const gart_settings* settings) {
+  g_err[0] = 0;
+  if (check_settings(settings) != GART_OK) return 0;
+  static const int32_t bytes[6] = {16, 4, 8, 2, 8, 2};
+  return bytes[lt_format_for(settings)];
+}
 
 size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, const gart_camera* camera,
                           const gart_settings* settings) {
@@ -349,7 +367,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.lt_offset = f->lt_offset;
   A.sh = g->sh;
   A.lt = reinterpret_cast<uint4*>(f->lt);
-  A.lt_t_only = settings->backward_mode == GART_BACKWARD_HYBRID;
+  A.lt_format = lt_format_for(settings);
   A.inv_color_step = 1.0 / f->color_step;
   A.image = image;
   A.pixel_state = f->pixel_state;
@@ -358,7 +376,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
   GART_HIP(launch_forward(A, s));
-  f->lt_format = A.lt_t_only ? GART_LT_T_ONLY : GART_LT_FULL;
+  f->lt_format = A.lt_format;
   f->stage = 3;
   return GART_OK;
 }
@@ -376,9 +394,9 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
-  GART_REQUIRE(f->lt_format == (settings->backward_mode == GART_BACKWARD_HYBRID ? GART_LT_T_ONLY : GART_LT_FULL),
-               "frame lt_format %d does not match backward mode %d (render with the same mode)", f->lt_format,
-               settings->backward_mode);
+  GART_REQUIRE(f->lt_format == lt_format_for(settings),
+               "frame lt_format %d does not match backward mode %d / lt_precision %d (render with the same settings)",
+               f->lt_format, settings->backward_mode, settings->lt_precision);
   if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
   const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode, settings->tile);
@@ -403,6 +421,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.tile_count = f->tile_count;
   A.sh = g->sh;
   A.lt = reinterpret_cast<const uint4*>(f->lt);
+  A.lt_format = f->lt_format;
   A.color_step = float(f->color_step);
   A.dl_dimage = dL_dimage;
   A.pixel_state = f->pixel_state;

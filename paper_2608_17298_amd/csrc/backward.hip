@@ -33,7 +33,7 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Adds the gradient contribution of one composited hit to acc (accumulator
 // layout), with explicit fused multiply-adds.
-template <int K>
+template <int K, int FMT>
 __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], double sigma, const float sh[3 * K],
                                              const float Y[K], const uint32_t Cq[3], const float g[3], uint4 lt,
                                              float step, float acc[acc_width(K)]) {
@@ -50,15 +50,14 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
     pos[ch] = v > 0.0f;
     c[ch] = pos[ch] ? v : 0.0f;
   }
-  const float T = __uint_as_float(lt.w);
-  const uint32_t Lq[3] = {lt.x, lt.y, lt.z};
+  const float T = lt_T<FMT>(lt);
   const float ta = T * a;
   const float inv = __builtin_amdgcn_rcpf(1.0f - a);  // about 1 ulp
   float dlda = 0.0f;
   float dc[3];
 #pragma unroll
   for (int ch = 0; ch < 3; ++ch) {
-    const float S = fmaf(-ta, c[ch], __uint2float_rn(Cq[ch] - Lq[ch]) * step);  // colour behind the hit
+    const float S = fmaf(-ta, c[ch], lt_c_minus_l<FMT>(lt, Cq, ch, step));  // colour behind the hit
     dlda = fmaf(g[ch], fmaf(T, c[ch], -S * inv), dlda);
     dc[ch] = pos[ch] ? ta * g[ch] : 0.0f;
   }
@@ -155,10 +154,10 @@ __device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint3
   return kept;
 }
 
-template <int TILE, int K, bool ATOMIC, bool HYBRID>
+template <int TILE, int K, bool ATOMIC, bool HYBRID, int FMT>
 __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
-  // HYBRID: the intermediate buffer holds T only (4 bytes per entry) and the
-  // unit accumulates only the SH sums (the pixel pass adds the others).
+  // HYBRID: the intermediate buffer holds T only (FMT T_ONLY or T_HALF) and
+  // the unit accumulates only the SH sums (the pixel pass adds the others).
   constexpr int NT = TILE * TILE;
   constexpr int G = NT / 64;      // pixel groups (waves) per tile
   constexpr int R = 64 / TILE;    // tile rows per group
@@ -302,13 +301,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       // offset inside rect cap tile (Eq. 16).
       const int64_t base = A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, xa, ya) +
                            int64_t(oy + g * R - ya) * w + (ox - xa);
-      auto lt_at = [&](int b) {
-        const int64_t e = base + int64_t(b / TILE) * w + (b % TILE);
-        if constexpr (HYBRID)
-          return make_uint4(0, 0, 0, __float_as_uint(reinterpret_cast<const float*>(A.lt)[e]));
-        else
-          return A.lt[e];
-      };
+      auto lt_at = [&](int b) { return lt_load<FMT>(A.lt, base + int64_t(b / TILE) * w + (b % TILE)); };
       float acc[AW];
 #pragma unroll
       for (int v = 0; v < AW; ++v) acc[v] = 0.0f;
@@ -351,9 +344,9 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
           const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
           const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
           if constexpr (HYBRID)
-            hit_sh_acc<K>(D2, sigma, sh, Y, gr, __uint_as_float(lv[t].w), acc);
+            hit_sh_acc<K>(D2, sigma, sh, Y, gr, lt_T<FMT>(lv[t]), acc);
           else
-            hit_grad_acc<K>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
+            hit_grad_acc<K, FMT>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
         }
       }
       ++n_active;
@@ -405,7 +398,7 @@ struct HybridWindow {
   static constexpr int kWin = TILE == 8 ? 384 : 128;  // list positions per window
 };
 
-template <int TILE, int K>
+template <int TILE, int K, int FMT>
 __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A) {
   constexpr int NT = TILE * TILE;
   constexpr int G = HybridWindow<TILE>::G, kWin = HybridWindow<TILE>::kWin;
@@ -455,7 +448,7 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
       for (int e = 0; e < 3; ++e) og[e] = Gm[kGeoOg + e];
       const double sigma = Gm[kGeoSigma];
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
-      const float T = reinterpret_cast<const float*>(A.lt)[A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py)];
+      const float T = lt_T<FMT>(lt_load<FMT>(A.lt, A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py)));
       double D2, xg[3];
       hit_point(W, og, d, &D2, xg);
       const float rho = __builtin_amdgcn_exp2f(float(-0.72134752044448170368 * D2));
@@ -529,7 +522,7 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
 // Scatter control: one lane per pixel walks the tile's list front to back
 // and adds every composited hit's gradient with float atomics.
 // ---------------------------------------------------------------------------
-template <int TILE, int K>
+template <int TILE, int K, int FMT>
 __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
   constexpr int NT = TILE * TILE;
   constexpr int AW = acc_width(K), AS = acc_stride(K);
@@ -603,7 +596,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
         if (key_less(tend, iend, tau, id)) continue;
         ++n_hits;
         const int64_t li = __double_as_longlong(row[15]) + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py);
-        const uint4 lt = A.lt[li];
+        const uint4 lt = lt_load<FMT>(A.lt, li);
         float sh[3 * K];
         const float* shp = A.sh + int64_t(id) * (3 * K);
 #pragma unroll
@@ -611,7 +604,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
         float h[AW];
 #pragma unroll
         for (int v = 0; v < AW; ++v) h[v] = 0.0f;
-        hit_grad_acc<K>(D2, xg, row[13], sh, Y, Cq, g, lt, A.color_step, h);
+        hit_grad_acc<K, FMT>(D2, xg, row[13], sh, Y, Cq, g, lt, A.color_step, h);
         float* dst = A.acc + int64_t(id) * AS;
 #pragma unroll
         for (int v = 0; v < AW; ++v) unsafeAtomicAdd(dst + v, h[v]);
@@ -765,16 +758,52 @@ hipError_t launch_tk(const BackwardArgs& args, hipStream_t s) {
   if (!rows && (e = fill_f32(a.acc, 0.0f, a.n * AS, s)) != hipSuccess) return e;
   if ((e = record(a.ev[0], s)) != hipSuccess) return e;
   if (n_tiles > 0) {
-    if (a.mode == GART_BACKWARD_GATHER) {
-      gather_kernel<TILE, K, false, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
-    } else if (a.mode == GART_BACKWARD_GATHER_ATOMIC) {
-      gather_kernel<TILE, K, true, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
-    } else if (hybrid) {
-      gather_kernel<TILE, K, false, true><<<n_tiles, TILE * TILE, 0, s>>>(a);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-      hybrid_pixel_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
-    } else {
-      scatter_kernel<TILE, K><<<n_tiles, TILE * TILE, 0, s>>>(a);
+    switch (a.mode) {
+      case GART_BACKWARD_GATHER:
+        switch (a.lt_format) {
+          case GART_LT_FULL: gather_kernel<TILE, K, false, false, GART_LT_FULL><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_HALF: gather_kernel<TILE, K, false, false, GART_LT_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_FIXED16: gather_kernel<TILE, K, false, false, GART_LT_FIXED16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          default: return hipErrorInvalidValue;
+        }
+        break;
+      case GART_BACKWARD_GATHER_ATOMIC:
+        switch (a.lt_format) {
+          case GART_LT_FULL: gather_kernel<TILE, K, true, false, GART_LT_FULL><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_HALF: gather_kernel<TILE, K, true, false, GART_LT_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_FIXED16: gather_kernel<TILE, K, true, false, GART_LT_FIXED16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          default: return hipErrorInvalidValue;
+        }
+        break;
+      case GART_BACKWARD_SCATTER:
+        switch (a.lt_format) {
+          case GART_LT_FULL: scatter_kernel<TILE, K, GART_LT_FULL><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_HALF: scatter_kernel<TILE, K, GART_LT_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_FIXED16: scatter_kernel<TILE, K, GART_LT_FIXED16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          default: return hipErrorInvalidValue;
+        }
+        break;
+      case GART_BACKWARD_HYBRID:
+        switch (a.lt_format) {
+          case GART_LT_T_ONLY:
+            gather_kernel<TILE, K, false, true, GART_LT_T_ONLY><<<n_tiles, TILE * TILE, 0, s>>>(a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hybrid_pixel_kernel<TILE, K, GART_LT_T_ONLY><<<n_tiles, TILE * TILE, 0, s>>>(a);
+            break;
+          case GART_LT_T_HALF:
+            gather_kernel<TILE, K, false, true, GART_LT_T_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hybrid_pixel_kernel<TILE, K, GART_LT_T_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a);
+            break;
+          case GART_LT_T_LOG16:
+            gather_kernel<TILE, K, false, true, GART_LT_T_LOG16><<<n_tiles, TILE * TILE, 0, s>>>(a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hybrid_pixel_kernel<TILE, K, GART_LT_T_LOG16><<<n_tiles, TILE * TILE, 0, s>>>(a);
+            break;
+          default: return hipErrorInvalidValue;
+        }
+        break;
+      default: return hipErrorInvalidValue;
     }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -164,6 +164,72 @@ __device__ __forceinline__ uint32_t color_fixed(double v, double inv_step) {
   return uint32_t(fmin(rint(v * inv_step), 4294967295.0));
 }
 
+// fp16 storage of intermediate-buffer values: float rounded to the nearest
+// fp16 (hardware conversion), and back.
+__device__ __forceinline__ uint32_t half_bits(float x) {
+  return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));
+}
+__device__ __forceinline__ float half_value(uint32_t bits) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits & 0xffffu)));
+}
+
+// 16-bit logarithmic code of a transmittance T in (0, 1]: 4096 codes per
+// octave, q = round(-log2(T) * 4096) (saturating), T = 2^(-q / 4096); the
+// relative error is at most 2^(1/8192) - 1 = 8.5e-5 (hardware log2 / exp2).
+__device__ __forceinline__ uint32_t t_log16(float T) {
+  return uint32_t(fminf(rintf(-__builtin_amdgcn_logf(T) * 4096.0f), 65535.0f));
+}
+__device__ __forceinline__ float t_from_log16(uint32_t q) {
+  return __builtin_amdgcn_exp2f(float(q & 0xffffu) * (-1.0f / 4096.0f));
+}
+
+// Loads intermediate-buffer entry e in layout FMT (gart_lt_format) into a
+// uint4 container: FULL as stored; T_ONLY, T_HALF and T_LOG16 with the T
+// bits in .w; HALF and FIXED16 with their two words in .x (L.r | L.g << 16)
+// and .y (L.b | T << 16).
+template <int FMT>
+__device__ __forceinline__ uint4 lt_load(const uint4* lt, int64_t e) {
+  if constexpr (FMT == GART_LT_FULL) {
+    return lt[e];
+  } else if constexpr (FMT == GART_LT_T_ONLY) {
+    return make_uint4(0u, 0u, 0u, reinterpret_cast<const uint32_t*>(lt)[e]);
+  } else if constexpr (FMT == GART_LT_HALF || FMT == GART_LT_FIXED16) {
+    const uint2 v = reinterpret_cast<const uint2*>(lt)[e];
+    return make_uint4(v.x, v.y, 0u, 0u);
+  } else {
+    return make_uint4(0u, 0u, 0u, uint32_t(reinterpret_cast<const uint16_t*>(lt)[e]));
+  }
+}
+
+// Transmittance in front of the hit, from a loaded entry.
+template <int FMT>
+__device__ __forceinline__ float lt_T(uint4 v) {
+  if constexpr (FMT == GART_LT_FULL || FMT == GART_LT_T_ONLY) return __uint_as_float(v.w);
+  else if constexpr (FMT == GART_LT_HALF) return half_value(v.y >> 16);
+  else if constexpr (FMT == GART_LT_T_HALF) return half_value(v.w);
+  else if constexpr (FMT == GART_LT_FIXED16) return t_from_log16(v.y >> 16);
+  else return t_from_log16(v.w);
+}
+
+// C - L of channel ch (final colour minus the colour in front of the hit),
+// from the pixel's fixed-point C and a loaded FULL, HALF or FIXED16 entry.
+// FULL and FIXED16: an exact integer difference in units of step (the 16-bit
+// L is in units of step * 2^16), then one rounding; HALF: C (float) minus the
+// fp16 L.
+template <int FMT>
+__device__ __forceinline__ float lt_c_minus_l(uint4 v, const uint32_t Cq[3], int ch, float step) {
+  if constexpr (FMT == GART_LT_FULL) {
+    const uint32_t Lq = ch == 0 ? v.x : (ch == 1 ? v.y : v.z);
+    return __uint2float_rn(Cq[ch] - Lq) * step;
+  } else {
+    const uint32_t hb = ch == 0 ? v.x : (ch == 1 ? (v.x >> 16) : v.y);
+    if constexpr (FMT == GART_LT_FIXED16)
+      return float(int64_t(Cq[ch]) - int64_t(hb & 0xffffu) * 65536) * step;
+    else
+      return __uint2float_rn(Cq[ch]) * step - half_value(hb);
+  }
+}
+
 // Adds a per-lane count to a device counter with one atomic per wave.  Must
 // be called with the whole wave active.
 __device__ __forceinline__ void count_add(uint64_t* ctr, uint32_t v) {

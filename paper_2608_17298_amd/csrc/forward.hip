@@ -35,7 +35,7 @@ constexpr int kMaxPasses = 1 << 20;
 // row: [0..8] W, [9..11] o_g, [12] D2c, [13] sigma, [14] depth key,
 // [15] O_prim (int64 bits), [16..17] rect (4 x int32), [18] index (uint32)
 
-template <int TILE, int K, bool T_ONLY>
+template <int TILE, int K, int FMT>
 __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int NT = TILE * TILE;
   constexpr int KB = GART_FWD_KB;  // per-lane hit buffer (registers)
@@ -122,11 +122,25 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     // k-th composited hit of this pixel -> its list position (read by the
     // gather backward)
     A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = bc[0];
-    if constexpr (T_ONLY)
-      reinterpret_cast<float*>(A.lt)[lt_base + bi[0]] = float(T);
-    else
-      A.lt[lt_base + bi[0]] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
-                                         color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
+    const int64_t e = lt_base + bi[0];
+    if constexpr (FMT == GART_LT_FULL) {
+      A.lt[e] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
+                           color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
+    } else if constexpr (FMT == GART_LT_T_ONLY) {
+      reinterpret_cast<float*>(A.lt)[e] = float(T);
+    } else if constexpr (FMT == GART_LT_HALF) {
+      reinterpret_cast<uint2*>(A.lt)[e] = make_uint2(half_bits(float(L0)) | (half_bits(float(L1)) << 16),
+                                                     half_bits(float(L2)) | (half_bits(float(T)) << 16));
+    } else if constexpr (FMT == GART_LT_FIXED16) {
+      const double inv16 = A.inv_color_step * (1.0 / 65536.0);
+      reinterpret_cast<uint2*>(A.lt)[e] = make_uint2(
+          min(color_fixed(L0, inv16), 65535u) | (min(color_fixed(L1, inv16), 65535u) << 16),
+          min(color_fixed(L2, inv16), 65535u) | (t_log16(float(T)) << 16));
+    } else if constexpr (FMT == GART_LT_T_LOG16) {
+      reinterpret_cast<uint16_t*>(A.lt)[e] = uint16_t(t_log16(float(T)));
+    } else {
+      reinterpret_cast<uint16_t*>(A.lt)[e] = uint16_t(half_bits(float(T)));
+    }
     const double w = T * a;
     L0 = fma(w, double(c[0]), L0);
     L1 = fma(w, double(c[1]), L1);
@@ -306,10 +320,15 @@ hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
   const int n_tiles = a.tiles_x * a.tiles_y;
   hipError_t e = record(a.ev_begin, s);
   if (e != hipSuccess) return e;
-  if (a.lt_t_only)
-    forward_kernel<TILE, K, true><<<n_tiles, TILE * TILE, 0, s>>>(a);
-  else
-    forward_kernel<TILE, K, false><<<n_tiles, TILE * TILE, 0, s>>>(a);
+  switch (a.lt_format) {
+    case GART_LT_FULL: forward_kernel<TILE, K, GART_LT_FULL><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_T_ONLY: forward_kernel<TILE, K, GART_LT_T_ONLY><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_HALF: forward_kernel<TILE, K, GART_LT_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_T_HALF: forward_kernel<TILE, K, GART_LT_T_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_FIXED16: forward_kernel<TILE, K, GART_LT_FIXED16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_T_LOG16: forward_kernel<TILE, K, GART_LT_T_LOG16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(a.ev_end, s);
 }

@@ -95,8 +95,8 @@ struct ForwardArgs {
   const int32_t* rect;
   const int64_t* lt_offset;
   const float* sh;
-  uint4* lt;                // (L fixed point, T bits) entries, or float T only
-  bool lt_t_only;           // write T only (4-byte entries, hybrid backward)
+  uint4* lt;                // entries in the layout lt_format names
+  int lt_format;            // gart_lt_format
   double inv_color_step;    // fixed-point units per unit of colour
   float* image;
   gart_pixel_state* pixel_state;
@@ -120,7 +120,8 @@ struct BackwardArgs {
   const int64_t* pair_offset;
   const uint32_t* tile_count;
   const float* sh;
-  const uint4* lt;          // (L fixed point, T bits) entries; float T only in hybrid mode
+  const uint4* lt;          // entries in the layout lt_format names
+  int lt_format;            // gart_lt_format
   float color_step;         // colour per fixed-point unit (a power of two times a float)
   const float* dl_dimage;
   const gart_pixel_state* pixel_state;

@@ -34,7 +34,9 @@ GATHER_ATOMIC = 1
 SCATTER = 2
 HYBRID = 3
 MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER, "hybrid": HYBRID}
-LT_FULL, LT_T_ONLY = 0, 1
+LT_FULL, LT_T_ONLY, LT_HALF, LT_T_HALF, LT_FIXED16, LT_T_LOG16 = 0, 1, 2, 3, 4, 5
+LT_PRECISION_FULL, LT_PRECISION_HALF, LT_PRECISION_FIXED16 = 0, 1, 2
+PRECISIONS = {"full": LT_PRECISION_FULL, "half": LT_PRECISION_HALF, "fixed16": LT_PRECISION_FIXED16}
 
 CNT_FWD_HITS, CNT_FWD_TESTS, CNT_FWD_RESCANS = 0, 1, 2
 CNT_BWD_HITS, CNT_BWD_TESTS, CNT_BWD_ATOMICS, CNT_BWD_PAIRS, CNT_BWD_ACTIVE = 3, 4, 5, 6, 7
@@ -60,7 +62,7 @@ class gart_gaussians(ctypes.Structure):
 
 class gart_settings(ctypes.Structure):
     _fields_ = [("alpha_min", ctypes.c_float), ("t_min", ctypes.c_float), ("tile", ctypes.c_int32),
-                ("backward_mode", ctypes.c_int32)]
+                ("backward_mode", ctypes.c_int32), ("lt_precision", ctypes.c_int32)]
 
 
 class gart_frame(ctypes.Structure):
@@ -99,6 +101,8 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         L.gart_scratch_bytes.restype = ctypes.c_size_t
         L.gart_scratch_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int64, _P, _P]
+        L.gart_lt_entry_bytes.restype = ctypes.c_int32
+        L.gart_lt_entry_bytes.argtypes = [_P]
         L.gart_bounds.restype = ctypes.c_int
         L.gart_bounds.argtypes = [_P, _P, _P, _P, _P, _P, _P]
         L.gart_build_tile_map.restype = ctypes.c_int
@@ -164,13 +168,22 @@ def make_camera(cam) -> gart_camera:
     return c
 
 
-def make_settings(tile=8, backward_mode=GATHER, alpha_min=None, t_min=None) -> gart_settings:
+def make_settings(tile=8, backward_mode=GATHER, alpha_min=None, t_min=None, lt_precision=LT_PRECISION_FULL) -> gart_settings:
     s = gart_settings()
     s.alpha_min = float(1.0 / 255.0) if alpha_min is None else float(alpha_min)
     s.t_min = 1e-4 if t_min is None else float(t_min)
     s.tile = int(tile)
     s.backward_mode = MODES[backward_mode] if isinstance(backward_mode, str) else int(backward_mode)
+    s.lt_precision = PRECISIONS[lt_precision] if isinstance(lt_precision, str) else int(lt_precision)
     return s
+
+
+def gart_lt_entry_bytes(settings: gart_settings) -> int:
+    """Bytes per intermediate-buffer entry that gart_forward writes for these settings."""
+    n = int(lib().gart_lt_entry_bytes(ctypes.byref(settings)))
+    if n <= 0:
+        raise GartError(GART_ERR_INVALID_ARG, "gart_lt_entry_bytes", lib().gart_last_error().decode())
+    return n
 
 
 @dataclass
@@ -239,10 +252,11 @@ class Frame:
         self._alloc_pairs(pair_capacity)
 
     def _alloc_lt(self, cap):
-        # gart_lt_entry: three fixed-point colour words and the float bits of
-        # T; the hybrid backward's forward writes T only (one word)
-        words = 1 if self.settings.backward_mode == HYBRID else 4
-        self.lt = torch.empty((max(int(cap), 1), words), dtype=torch.int32, device=self.device)
+        # entries of gart_lt_entry_bytes(settings) bytes, held as int16 words
+        # (16 bytes: fixed-point L and float T; 4: float T; 8: fp16 L and T;
+        # 2: fp16 T)
+        words = gart_lt_entry_bytes(self.settings) // 2
+        self.lt = torch.empty((max(int(cap), 1), words), dtype=torch.int16, device=self.device)
         self.lt_capacity = int(cap)
 
     def _alloc_pairs(self, cap):
@@ -255,7 +269,8 @@ class Frame:
         # sized for every backward mode, so one frame serves all of them
         nbytes = 0
         for mode in (GATHER, GATHER_ATOMIC, SCATTER, HYBRID):
-            st = gart_settings(self.settings.alpha_min, self.settings.t_min, self.settings.tile, mode)
+            st = gart_settings(self.settings.alpha_min, self.settings.t_min, self.settings.tile, mode,
+                               self.settings.lt_precision)
             nbytes = max(nbytes, gart_scratch_bytes(self.n, self.sh_degree, cap, self.camera, st))
         self.scratch = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
 
@@ -298,12 +313,23 @@ class Frame:
 
     def lt_entries_host(self, index: torch.Tensor):
         """(L [m,3] float64, T [m] float32) of the listed (L,T) entries, on
-        the host; L is None for a T-only buffer (hybrid backward)."""
-        raw = self.lt[index].cpu().numpy()
-        if int(self.c.lt_format) == LT_T_ONLY:
-            return None, raw[:, 0].copy().view(np.float32)
-        L = raw[:, :3].view(np.uint32).astype(np.float64) * self.color_step
-        return L, raw[:, 3].copy().view(np.float32)
+        the host, decoded from the frame's lt_format; L is None for a T-only
+        buffer (hybrid backward)."""
+        raw = np.ascontiguousarray(self.lt[index].cpu().numpy())
+        fmt = int(self.c.lt_format)
+        if fmt == LT_T_ONLY:
+            return None, raw.view(np.float32)[:, 0].copy()
+        if fmt == LT_T_HALF:
+            return None, raw.view(np.float16)[:, 0].astype(np.float32)
+        if fmt == LT_HALF:
+            h = raw.view(np.float16)
+            return h[:, :3].astype(np.float64), h[:, 3].astype(np.float32)
+        if fmt in (LT_FIXED16, LT_T_LOG16):
+            u = raw.view(np.uint16).astype(np.float64)
+            T = np.exp2(-u[:, -1] / 4096.0).astype(np.float32)
+            return (None if fmt == LT_T_LOG16 else u[:, :3] * self.color_step * 65536.0), T
+        w = raw.view(np.uint32)
+        return w[:, :3].astype(np.float64) * self.color_step, w[:, 3].copy().view(np.float32)
 
     def pixel_state_host(self) -> dict:
         """gart_pixel_state fields of every pixel, on the host."""
@@ -347,10 +373,10 @@ def gart_forward(g: Gaussians, camera: gart_camera, settings: gart_settings, fra
     """Forward trace (Sec. 3.2-3.3, 4.3); image is [H,W,3] float32."""
     if image.dtype != torch.float32 or image.shape != (camera.height, camera.width, 3):
         raise ValueError("image must be float32 [H,W,3]")
-    if settings.backward_mode != HYBRID and frame.lt.shape[1] != 4:
-        # lt_capacity counts entries of the format this call writes
-        raise ValueError("frame's intermediate buffer holds T only (allocated for the hybrid backward); "
-                         "a 16-byte-entry render needs a frame allocated for another mode")
+    if frame.lt.shape[1] * 2 < gart_lt_entry_bytes(settings):
+        # lt_capacity counts entries of the size this call writes
+        raise ValueError(f"frame's intermediate buffer has {frame.lt.shape[1] * 2}-byte entries; these settings "
+                         f"write {gart_lt_entry_bytes(settings)}-byte entries (allocate the frame for them)")
     gs = g.c_struct()
     fs = frame.c_struct()
     _check(lib().gart_forward(ctypes.byref(gs), ctypes.byref(camera), ctypes.byref(settings), ctypes.byref(fs),

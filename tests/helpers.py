@@ -61,12 +61,12 @@ def l1_upstream(scene, oracle_mod):
     return np.sign(C - Cs).reshape(scene.camera.height, scene.camera.width, 3).astype(np.float32)
 
 
-def run_gpu(scene, mode="gather", tile=None, dl=None, counters=True, keep_frame=False):
+def run_gpu(scene, mode="gather", tile=None, dl=None, counters=True, keep_frame=False, precision="full"):
     """Run the four C-ABI calls on cuda:0 and return host copies of the outputs."""
     import torch
     from paper_2608_17298_amd import gart
     cam = gart.make_camera(scene.camera)
-    st = gart.make_settings(tile or scene.tile, mode)
+    st = gart.make_settings(tile or scene.tile, mode, lt_precision=precision)
     g = gart.Gaussians.from_scene(scene)
     frame = gart.prepare(g, cam, st, counters=counters)
     image = torch.empty((cam.height, cam.width, 3), dtype=torch.float32, device="cuda")

@@ -47,7 +47,7 @@ def _structs(tile=8, mode=0, n=0, deg=0, w=16, h=16):
     return cam, st, g, f
 
 
-@pytest.mark.parametrize("bad", ["tile", "mode", "alpha", "tmin", "width", "fx", "deg", "nptr", "frame"])
+@pytest.mark.parametrize("bad", ["tile", "mode", "precision", "alpha", "tmin", "width", "fx", "deg", "nptr", "frame"])
 def test_invalid_arguments_rejected_on_host(lib, bad):
     cam, st, g, f = _structs()
     fp = ctypes.byref(f)
@@ -55,6 +55,8 @@ def test_invalid_arguments_rejected_on_host(lib, bad):
         st.tile = 12
     elif bad == "mode":
         st.backward_mode = 5
+    elif bad == "precision":
+        st.lt_precision = 2
     elif bad == "alpha":
         st.alpha_min = 0.0
     elif bad == "tmin":
@@ -124,3 +126,17 @@ def test_ctypes_structs_match_header(tmp_path):
         for f in s._fields_:
             assert got[(s.__name__, f[0])] == getattr(s, f[0]).offset, (s.__name__, f[0])
     assert got[("gart_pixel_state", "size")] == 32 and got[("gart_lt_entry", "size")] == 16
+
+
+def test_lt_entry_bytes(lib):
+    """Entry size per (mode, precision): 16 / 4 (hybrid) bytes at full
+    precision, 8 / 2 with fp16 storage; 0 for invalid settings."""
+    from paper_2608_17298_amd import gart
+    want = {("gather", "full"): 16, ("gather_atomic", "full"): 16, ("scatter", "full"): 16, ("hybrid", "full"): 4,
+            ("gather", "half"): 8, ("gather_atomic", "half"): 8, ("scatter", "half"): 8, ("hybrid", "half"): 2}
+    for (mode, prec), nb in want.items():
+        assert gart.gart_lt_entry_bytes(gart.make_settings(8, mode, lt_precision=prec)) == nb, (mode, prec)
+    st = gart.make_settings(8, "gather")
+    st.lt_precision = 7
+    assert lib.gart_lt_entry_bytes(ctypes.byref(st)) == 0
+    assert lib.gart_lt_entry_bytes(None) == 0
