@@ -21,10 +21,10 @@ namespace gart {
 namespace {
 
 #ifndef GART_FWD_KB
-#define GART_FWD_KB 12
+#define GART_FWD_KB 16
 #endif
 #ifndef GART_FWD_FLUSH
-#define GART_FWD_FLUSH 4
+#define GART_FWD_FLUSH 16
 #endif
 
 constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
@@ -76,9 +76,12 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   double end_tau = kInf;
   uint32_t end_id = kNoPrim;
 
+  // Hit buffer: depth, alpha, tile-list position and Gaussian index of each
+  // pending hit, sorted by (depth, index); the (L,T) address is recomputed
+  // from the Gaussian's rectangle when the hit is composited, which keeps an
+  // entry at six registers.
   double bt[KB], ba[KB];
-  uint32_t bi[KB];  // (L,T) offset inside the Gaussian's block
-  uint32_t bid[KB], bc[KB];
+  uint32_t bc[KB], bid[KB];
   int cnt = 0;
   double e_tau = kInf;  // smallest dropped hit (all buffered hits are smaller)
   uint32_t e_id = kNoPrim;
@@ -87,9 +90,8 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   for (int s = 0; s < KB; ++s) {
     bt[s] = kInf;
     ba[s] = 0.0;
-    bi[s] = 0;
-    bid[s] = kNoPrim;
     bc[s] = 0;
+    bid[s] = kNoPrim;
   }
 
   auto drop = [&](double t, uint32_t id, uint32_t c) {
@@ -105,7 +107,8 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     const double a = ba[0];
     const uint32_t id = bid[0];
     const float* shp = A.sh + int64_t(id) * (3 * K);
-    const int64_t lt_base = A.lt_offset[id];
+    const int4 rr = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
+    const int64_t lt_base = A.lt_offset[id] + lt_local_index(rr.x, rr.y, rr.z, rr.w, TILE, px, py);
     float c[3] = {0.5f, 0.5f, 0.5f};
 #pragma unroll
     for (int k = 0; k < KP; k += 4) {
@@ -122,7 +125,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     // k-th composited hit of this pixel -> its list position (read by the
     // gather backward)
     A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = bc[0];
-    const int64_t e = lt_base + bi[0];
+    const int64_t e = lt_base;
     if constexpr (FMT == GART_LT_FULL) {
       A.lt[e] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
                            color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
@@ -158,9 +161,8 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     for (int s = 0; s + 1 < KB; ++s) {
       bt[s] = bt[s + 1];
       ba[s] = ba[s + 1];
-      bi[s] = bi[s + 1];
-      bid[s] = bid[s + 1];
       bc[s] = bc[s + 1];
+      bid[s] = bid[s + 1];
     }
     --cnt;
   };
@@ -222,7 +224,6 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
                 }
                 if (ins) {
                   const double a = row[13] * exp(-0.5 * D2);
-                  const uint32_t li = uint32_t(lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py));
                   int pos = 0;
 #pragma unroll
                   for (int s = 0; s < KB; ++s) pos += (s < cnt && key_less(bt[s], bid[s], tau, id)) ? 1 : 0;
@@ -231,9 +232,8 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
                     if (s > pos && s <= cnt) {
                       bt[s] = bt[s - 1];
                       ba[s] = ba[s - 1];
-                      bi[s] = bi[s - 1];
-                      bid[s] = bid[s - 1];
                       bc[s] = bc[s - 1];
+                      bid[s] = bid[s - 1];
                     }
                   }
 #pragma unroll
@@ -241,9 +241,8 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
                     if (s == pos) {
                       bt[s] = tau;
                       ba[s] = a;
-                      bi[s] = li;
-                      bid[s] = id;
                       bc[s] = cpos;
+                      bid[s] = id;
                     }
                   }
                   ++cnt;
@@ -251,10 +250,11 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
               }
             }
           }
-          // Composite the final hits every kFlushEvery Gaussians (so that each
-          // compositing step serves more lanes), at the end of a batch, and
-          // whenever the buffer is full.
-          if ((c + 1) % kFlushEvery == 0 || c + 1 == nb || cnt == KB) {
+          // Composite the final hits every kFlushEvery Gaussians, at the end
+          // of a batch, and whenever a lane's buffer is full -- for every
+          // lane of the wave at once, so that each compositing step serves
+          // more lanes.
+          if (__ballot((c + 1) % kFlushEvery == 0 || c + 1 == nb || cnt == KB) != 0) {
             const double nk = double(s_key[c + 1]);
             while (cnt > 0 && bt[0] < nk && !done) composite_front();
             if (done) break;
