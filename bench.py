@@ -43,7 +43,7 @@ GEOM_BYTES = 128 + 16 + 8 + 4  # per staged pair in the forward: fp64 geometry r
 UNIT_BYTES = 104 + 8 + 16 + 8 + 8  # per gather unit: W and o_g, sigma, rect, O_prim, pair offset
 
 
-ALL_MODES = ("gather", "gather_atomic", "scatter", "hybrid")
+ALL_MODES = ("gather", "gather_wave", "gather_atomic", "scatter", "hybrid")
 # backward mode + intermediate-buffer precision pairs timed beside the default
 STORAGE_VARIANTS = (("gather", "fixed16"), ("gather", "half"), ("hybrid", "fixed16"))
 
@@ -304,6 +304,7 @@ def main():
             modes[mode] = dict(backward_ms=round(bms, 4), main_kernel_ms=round(kms, 4),
                                grads_per_s=round(int(cm[gart.CNT_BWD_HITS]) / (bms * 1e-3), 1),
                                float_atomics=int(cm[gart.CNT_BWD_ATOMICS]),
+                               wave_units=int(cm[gart.CNT_BWD_WAVE_UNITS]),
                                lt_bytes=int(frame.lt_entries) * gart.gart_lt_entry_bytes(stm))
         for mode, prec in STORAGE_VARIANTS:
             stm = gart.make_settings(sc.tile, mode, lt_precision=prec)
@@ -347,7 +348,7 @@ def main():
         "forward_rescans": int(c[gart.CNT_FWD_RESCANS]),
         "counters": {name: int(c[i]) for i, name in enumerate(
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
-             "bwd_active_units", "fwd_drops", "bwd_hybrid_steps"])},
+             "bwd_active_units", "fwd_drops", "bwd_hybrid_steps", "bwd_wave_units"])},
         "kernels_roofline": {k: with_counters(k) for k in work},
         "train_step": train,
     }

@@ -62,8 +62,10 @@ typedef enum {
   GART_BACKWARD_GATHER = 0,        /* (tile, prim) pairs -> per-pair rows -> one reduction per primitive */
   GART_BACKWARD_GATHER_ATOMIC = 1, /* (tile, prim) pairs -> one atomic update per pair (Sec. 4.4 as printed) */
   GART_BACKWARD_SCATTER = 2,       /* pixel-centric control: one atomic update per composited hit (Sec. 3.5) */
-  GART_BACKWARD_HYBRID = 3         /* Sec. 4.4 "Hybrid approach": SH sums gathered per pair, the other 10 sums
+  GART_BACKWARD_HYBRID = 3,        /* Sec. 4.4 "Hybrid approach": SH sums gathered per pair, the other 10 sums
                                       scattered per hit from a back-to-front walk; lt holds T only (4 B) */
+  GART_BACKWARD_GATHER_WAVE = 4    /* GATHER, with units of >= 48 hits evaluated by a whole wave, one lane per
+                                      pixel (Sec. 4.4, a warp per primitive) */
 } gart_backward_mode;
 
 /* Layout of gart_frame.lt, chosen by gart_forward from settings->backward_mode
@@ -198,6 +200,7 @@ enum {
   GART_CNT_FWD_DROPS = 8,     /* forward hits dropped from a full hit buffer (found again by a rescan) */
   GART_CNT_BWD_STEPS = 9,     /* hits walked by the hybrid pixel pass (composited hits, once per window
                                  of list positions that the tile needs) */
+  GART_CNT_BWD_WAVE_UNITS = 10, /* units evaluated by a whole wave (GATHER_WAVE) */
   GART_NUM_COUNTERS = 16
 };
 
@@ -299,6 +302,10 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
  *     per-Gaussian accumulators with one atomic update per value.
  *   SCATTER: the pixel-centric control (Sec. 3.5): one lane per pixel, one
  *     atomic add per gradient value per composited hit.
+ *   GATHER_WAVE: as GATHER, but a unit with at least 48 composited hits is
+ *     evaluated by its whole wave, one lane per pixel, and its 10 + 3K sums
+ *     are formed by a cross-lane reduction (Sec. 4.4 discusses a warp per
+ *     primitive).  Deterministic.
  *   HYBRID (Sec. 4.4, hybrid approach): the SH sums (3K) are gathered per
  *     unit into rows as in GATHER; a second kernel walks each pixel's
  *     composited hits back to front (hit_list), forms the colour behind

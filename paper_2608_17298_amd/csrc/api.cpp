@@ -64,7 +64,7 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
   L.totals = take(64);
   L.partials = take(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
   const size_t AS = size_t(acc_stride(K));
-  const bool rows = mode == GART_BACKWARD_GATHER || mode == GART_BACKWARD_HYBRID;
+  const bool rows = mode == GART_BACKWARD_GATHER || mode == GART_BACKWARD_GATHER_WAVE || mode == GART_BACKWARD_HYBRID;
   L.acc = take(rows ? 4 : size_t(nn) * AS * 4);
   const size_t rpp = size_t(tile) * size_t(tile) / 64;  // partial rows per pair (64-pixel groups)
   L.rows = take(rows ? size_t(pc) * rpp * AS * 4 : 4);
@@ -96,7 +96,7 @@ gart_status check_settings(const gart_settings* s) {
   GART_REQUIRE(s->alpha_min > 0.0f && s->alpha_min < 1.0f, "alpha_min must be in (0,1)");
   GART_REQUIRE(s->t_min > 0.0f && s->t_min < 1.0f, "t_min must be in (0,1)");
   GART_REQUIRE(s->tile == 8 || s->tile == 16, "tile must be 8 or 16");
-  GART_REQUIRE(s->backward_mode >= 0 && s->backward_mode <= 3, "unknown backward_mode %d", s->backward_mode);
+  GART_REQUIRE(s->backward_mode >= 0 && s->backward_mode <= 4, "unknown backward_mode %d", s->backward_mode);
   GART_REQUIRE(s->lt_precision >= GART_LT_PRECISION_FULL && s->lt_precision <= GART_LT_PRECISION_FIXED16,
                "unknown lt_precision %d", s->lt_precision);
   GART_REQUIRE(s->lt_precision != GART_LT_PRECISION_FIXED16 || s->t_min >= 0x1p-15f,

@@ -100,6 +100,28 @@ __device__ __forceinline__ void hit_sh_acc(double D2, double sigma, const float 
   }
 }
 
+// Sums v[0..31] over the 64 lanes of a wave; afterwards lanes l and l + 32
+// hold the total of value l (l < 32).  After one plain step across the two
+// half-waves, each halving step keeps half of the remaining values and adds
+// the partner lane's copy of them (63 cross-lane moves for 32 values,
+// against 32 x 6 for a plain reduction of each).
+__device__ __forceinline__ float wave_sum32_transposed(float* v) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int j = 0; j < 32; ++j) v[j] += __shfl_xor(v[j], 32);
+#pragma unroll
+  for (int half = 16; half >= 1; half >>= 1) {
+    const bool hi = lane & half;
+#pragma unroll
+    for (int j = 0; j < half; ++j) {
+      const float keep = hi ? v[half + j] : v[j];
+      const float send = hi ? v[j] : v[half + j];
+      v[j] = keep + __shfl_xor(send, half);
+    }
+  }
+  return v[0];
+}
+
 // ---------------------------------------------------------------------------
 // Gather: one workgroup per tile.  The tile's pixels form G = TILE^2 / 64
 // groups of 64 pixels (whole rows, one wave each); the unit of work is a
@@ -117,6 +139,10 @@ __device__ __forceinline__ void hit_sh_acc(double D2, double sigma, const float 
 // ---------------------------------------------------------------------------
 constexpr int kUnits = 512;  // units per LDS pass
 constexpr int kBatch = 8;    // composited hits whose (L,T) loads are issued together
+#ifndef GART_WAVE_MIN
+#define GART_WAVE_MIN 48
+#endif
+constexpr int kWaveMin = GART_WAVE_MIN;  // hits from which a unit is evaluated by its whole wave (mode GATHER_WAVE)
 
 // Per-pixel ray direction in LDS, padded to 32 bytes.
 struct __align__(16) RayRec {
@@ -129,7 +155,7 @@ struct __align__(16) RayRec {
 // return.  Returns the number of units kept.  Called by the whole block.
 template <int NT>
 __device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint32_t* s_hist, uint16_t* s_order,
-                                          uint32_t* s_total) {
+                                          uint32_t* s_total, int dense_min = 65, uint32_t* s_dense = nullptr) {
   __syncthreads();  // buckets and counts complete
   if (threadIdx.x < 64) {
     const uint32_t c = s_hist[threadIdx.x];
@@ -141,6 +167,9 @@ __device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint3
     }
     s_hist[threadIdx.x] = inc - c;
     if (threadIdx.x == 63) *s_total = inc;
+    // bucket b holds the units with 64 - b hits: those with >= dense_min
+    // hits are buckets 0 .. 64 - dense_min, the first entries of the order
+    if (s_dense && int(threadIdx.x) == 64 - dense_min) *s_dense = inc;
   }
   __syncthreads();
   for (int u = threadIdx.x; u < nu; u += NT) {
@@ -154,10 +183,13 @@ __device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint3
   return kept;
 }
 
-template <int TILE, int K, bool ATOMIC, bool HYBRID, int FMT>
-__global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
+template <int TILE, int K, bool ATOMIC, bool HYBRID, int FMT, bool WAVE = false>
+__global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
   // HYBRID: the intermediate buffer holds T only (FMT T_ONLY or T_HALF) and
   // the unit accumulates only the SH sums (the pixel pass adds the others).
+  // WAVE: units with at least kWaveMin hits are evaluated by their whole wave
+  // (one lane per pixel, then a cross-lane sum) before the others are dealt
+  // to single lanes.
   constexpr int NT = TILE * TILE;
   constexpr int G = NT / 64;      // pixel groups (waves) per tile
   constexpr int R = 64 / TILE;    // tile rows per group
@@ -171,6 +203,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
   __shared__ __align__(16) float s_cg[NT][8];  // C.rgb (fixed-point bits), g.rgb
   __shared__ uint32_t s_hist[64];
   __shared__ uint32_t s_total;
+  __shared__ uint32_t s_dense;
   __shared__ double s_wmax[G];
   __shared__ uint32_t s_red[G];
   __shared__ uint64_t s_mask[kUnits];
@@ -240,7 +273,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
 #pragma unroll
   for (int w = 0; w < G; ++w) vend += s_red[w];
 
-  uint32_t n_pairs = 0, n_hits = 0, n_atom = 0, n_active = 0;
+  uint32_t n_pairs = 0, n_hits = 0, n_atom = 0, n_active = 0, n_wave = 0;
   for (int64_t c0 = beg; c0 < vend; c0 += kPairs) {
     const int nc = int(min<int64_t>(kPairs, vend - c0));
     const int nu = nc * G;
@@ -277,9 +310,71 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
       s_bucket[u] = c ? uint8_t(64 - c) : uint8_t(0xff);
       if (c) atomicAdd(&s_hist[64 - c], 1u);
     }
-    const int nu2 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total);
+    const int nu2 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total, WAVE ? kWaveMin : 65, &s_dense);
 
-    for (int o = tid; o < nu2; o += NT) {
+    int o0 = 0;
+    if constexpr (WAVE) {
+      // Dense units, whole wave per unit: the wave of group g takes the dense
+      // units of its group; lane l is pixel l of the group.
+      const int nd = int(s_dense), wv = tid / 64, lane = tid % 64;
+      for (int o = 0; o < nd; ++o) {
+        const int u = __builtin_amdgcn_readfirstlane(int(s_order[o]));
+        if (u % G != wv) continue;
+        const uint32_t i = __builtin_amdgcn_readfirstlane(s_id[u / G]);
+        const bool has = (s_mask[u] >> lane) & 1ull;
+        const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
+        float v[64];
+#pragma unroll
+        for (int e = 0; e < 64; ++e) v[e] = 0.0f;
+        if (has) {
+          const double* Gm = A.geom + int64_t(kGeomStride) * i;
+          double W[9], og[3];
+#pragma unroll
+          for (int k = 0; k < 9; ++k) W[k] = Gm[k];
+#pragma unroll
+          for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
+          const double sigma = Gm[kGeoSigma];
+          float sh[3 * K];
+          const float* shp = A.sh + int64_t(i) * (3 * K);
+#pragma unroll
+          for (int k = 0; k < 3 * K; ++k) sh[k] = shp[k];
+          const int px = ox + tid % TILE, py = oy + tid / TILE;
+          const uint4 lt = lt_load<FMT>(A.lt, A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py));
+          double D2, xg[3];
+          hit_point(W, og, s_ray[tid].d, &D2, xg);
+          float Y[KP];
+#pragma unroll
+          for (int kk = 0; kk < KP; kk += 4) {
+            const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[tid][kk]);
+            Y[kk] = y4.x;
+            Y[kk + 1] = y4.y;
+            Y[kk + 2] = y4.z;
+            Y[kk + 3] = y4.w;
+          }
+          const uint4 c4 = *reinterpret_cast<const uint4*>(&s_cg[tid][0]);
+          const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[tid][4]);
+          const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
+          const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
+          hit_grad_acc<K, FMT>(D2, xg, sigma, sh, Y, Cq, gr, lt, A.color_step, v);  // v[0 .. AW)
+          ++n_hits;
+        }
+        // lane e < 32: sum of value e; lane e >= 32: sum of value e
+        const float lo = wave_sum32_transposed(v);
+        const float hi = wave_sum32_transposed(v + 32);
+        const float total = lane < 32 ? lo : hi;
+        const int tx0 = r.x / TILE, ty0 = r.y / TILE, tx1 = r.z / TILE;
+        const int64_t row = (A.pair_offset[i] + int64_t(ty - ty0) * (tx1 - tx0 + 1) + (tx - tx0)) * G + u % G;
+        if (lane < AS) A.rows[row * AS + lane] = lane < AW ? total : 0.0f;
+        if (lane == 0) {
+          A.row_flag[row] = 1;
+          ++n_active;
+          ++n_wave;
+        }
+      }
+      o0 = nd;
+    }
+
+    for (int o = o0 + tid; o < nu2; o += NT) {
       const int u = s_order[o], g = u % G;
       const uint32_t i = s_id[u / G];
       const double* Gm = A.geom + int64_t(kGeomStride) * i;
@@ -378,6 +473,7 @@ __global__ __launch_bounds__(TILE* TILE) void gather_kernel(BackwardArgs A) {
     count_add(A.counters + GART_CNT_BWD_ACTIVE, n_active);
     count_add(A.counters + GART_CNT_BWD_HITS, n_hits);
     count_add(A.counters + GART_CNT_BWD_ATOMICS, n_atom);
+    if constexpr (WAVE) count_add(A.counters + GART_CNT_BWD_WAVE_UNITS, n_wave);
   }
 }
 
@@ -753,7 +849,7 @@ hipError_t launch_tk(const BackwardArgs& args, hipStream_t s) {
   const int n_tiles = a.tiles_x * a.tiles_y;
   hipError_t e = hipSuccess;
   const bool hybrid = a.mode == GART_BACKWARD_HYBRID;
-  const bool rows = a.mode == GART_BACKWARD_GATHER || hybrid;
+  const bool rows = a.mode == GART_BACKWARD_GATHER || a.mode == GART_BACKWARD_GATHER_WAVE || hybrid;
   if (rows && (e = fill_u8(a.row_flag, 0, a.pair_count * a.rows_per_pair, s)) != hipSuccess) return e;
   if (!rows && (e = fill_f32(a.acc, 0.0f, a.n * AS, s)) != hipSuccess) return e;
   if ((e = record(a.ev[0], s)) != hipSuccess) return e;
@@ -764,6 +860,14 @@ hipError_t launch_tk(const BackwardArgs& args, hipStream_t s) {
           case GART_LT_FULL: gather_kernel<TILE, K, false, false, GART_LT_FULL><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
           case GART_LT_HALF: gather_kernel<TILE, K, false, false, GART_LT_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
           case GART_LT_FIXED16: gather_kernel<TILE, K, false, false, GART_LT_FIXED16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          default: return hipErrorInvalidValue;
+        }
+        break;
+      case GART_BACKWARD_GATHER_WAVE:
+        switch (a.lt_format) {
+          case GART_LT_FULL: gather_kernel<TILE, K, false, false, GART_LT_FULL, true><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_HALF: gather_kernel<TILE, K, false, false, GART_LT_HALF, true><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+          case GART_LT_FIXED16: gather_kernel<TILE, K, false, false, GART_LT_FIXED16, true><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
           default: return hipErrorInvalidValue;
         }
         break;

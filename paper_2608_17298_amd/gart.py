@@ -33,7 +33,9 @@ GATHER = 0
 GATHER_ATOMIC = 1
 SCATTER = 2
 HYBRID = 3
-MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER, "hybrid": HYBRID}
+GATHER_WAVE = 4
+MODES = {"gather": GATHER, "gather_atomic": GATHER_ATOMIC, "scatter": SCATTER, "hybrid": HYBRID,
+         "gather_wave": GATHER_WAVE}
 LT_FULL, LT_T_ONLY, LT_HALF, LT_T_HALF, LT_FIXED16, LT_T_LOG16 = 0, 1, 2, 3, 4, 5
 LT_PRECISION_FULL, LT_PRECISION_HALF, LT_PRECISION_FIXED16 = 0, 1, 2
 PRECISIONS = {"full": LT_PRECISION_FULL, "half": LT_PRECISION_HALF, "fixed16": LT_PRECISION_FIXED16}
@@ -42,6 +44,7 @@ CNT_FWD_HITS, CNT_FWD_TESTS, CNT_FWD_RESCANS = 0, 1, 2
 CNT_BWD_HITS, CNT_BWD_TESTS, CNT_BWD_ATOMICS, CNT_BWD_PAIRS, CNT_BWD_ACTIVE = 3, 4, 5, 6, 7
 CNT_FWD_DROPS = 8
 CNT_BWD_STEPS = 9
+CNT_BWD_WAVE_UNITS = 10
 NUM_COUNTERS = 16
 EV_SORT, EV_FWD, EV_BWD, EV_REDUCE = 0, 2, 4, 6  # begin index; end = begin + 1
 NUM_EVENTS = 8
@@ -268,7 +271,7 @@ class Frame:
         self.pair_capacity = cap
         # sized for every backward mode, so one frame serves all of them
         nbytes = 0
-        for mode in (GATHER, GATHER_ATOMIC, SCATTER, HYBRID):
+        for mode in (GATHER, GATHER_ATOMIC, SCATTER, HYBRID, GATHER_WAVE):
             st = gart_settings(self.settings.alpha_min, self.settings.t_min, self.settings.tile, mode,
                                self.settings.lt_precision)
             nbytes = max(nbytes, gart_scratch_bytes(self.n, self.sh_degree, cap, self.camera, st))

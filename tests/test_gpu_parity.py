@@ -130,7 +130,7 @@ def test_forward_lt_entries(name):
     assert np.abs(T.astype(np.float64) - LT[:, 3]).max() <= 1e-6
 
 
-@pytest.mark.parametrize("mode", ["gather", "gather_atomic", "scatter", "hybrid"])
+@pytest.mark.parametrize("mode", ["gather", "gather_wave", "gather_atomic", "scatter", "hybrid"])
 @pytest.mark.parametrize("name", SCENES)
 def test_backward_parity(name, mode):
     sc, o, info, ren, grads, gpu = _case(name, mode)
@@ -171,6 +171,26 @@ def test_hybrid_t_only_buffer(name):
     L, T = fr.lt_entries_host(torch.from_numpy(idx).cuda())
     assert L is None
     assert np.abs(T.astype(np.float64) - LT[:, 3]).max() <= 1e-6
+
+
+@pytest.mark.parametrize("name", ["tiny", "stress_reduced", "1m_reduced"])
+def test_gather_wave_units(name):
+    """GATHER_WAVE evaluates the units with at least 48 hits by a whole wave
+    (Sec. 4.4, a warp per primitive) and the rest per lane: the dense path
+    is taken where such units exist, every unit is still visited once, and
+    the gradients match the per-lane gather to float rounding."""
+    from paper_2608_17298_amd import gart
+    sc, o, info, ren, grads, gpu = _case(name, "gather_wave")
+    ref = _case(name, "gather")[5]
+    c, cr = gpu["counters"], ref["counters"]
+    assert c[gart.CNT_BWD_ACTIVE] == cr[gart.CNT_BWD_ACTIVE]
+    assert c[gart.CNT_BWD_HITS] == cr[gart.CNT_BWD_HITS]
+    if name == "stress_reduced":  # large footprints: many units cover most of their pixels
+        assert c[gart.CNT_BWD_WAVE_UNITS] > 0
+    assert c[gart.CNT_BWD_WAVE_UNITS] <= c[gart.CNT_BWD_ACTIVE]
+    for k in GROUPS:
+        assert rel_l2(gpu["grads"][k], ref["grads"][k]) <= 1e-6, k
+    assert gart.CNT_BWD_WAVE_UNITS == 10
 
 
 # Reduced-precision intermediate storage (Sec. 6 suggests fp16).  Bars:
