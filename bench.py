@@ -247,14 +247,15 @@ def main():
     # pair its index and depth bound; per (pair, group) unit with hits the
     # Gaussian's geometry and SH, one partial row and its flag; per pixel the
     # upstream gradient and pixel state.  forward: per composited hit the
-    # (L,T) entry and hit-list word written; per staged pair its geometry row;
-    # SH once per (tile, Gaussian) with hits; per pixel the image and state.
+    # (L,T) entry and hit-list word written; per pair of the visited prefix
+    # (the list up to the tile's last ray end) its geometry row; SH once per
+    # (tile, Gaussian) with hits; per pixel the image and state.
     work = {
         "backward_main": dict(
             bytes=20 * bwd_hits + 12 * bwd_pairs + bwd_active * (UNIT_BYTES + 12 * K + 4 * AS + 1) + npix * (12 + 32),
             f64=F64_PER_TEST * bwd_tests + F64_PER_HIT_BWD * bwd_hits, f32=f32_per_hit_bwd(K) * bwd_hits),
         "forward_trace": dict(
-            bytes=20 * hits + int(frame.pair_count) * GEOM_BYTES + bwd_active * 12 * K + npix * (12 + 32),
+            bytes=20 * hits + bwd_pairs * GEOM_BYTES + bwd_active * 12 * K + npix * (12 + 32),
             f64=F64_PER_TEST * fwd_tests + 30 * hits, f32=f32_per_hit_fwd(K) * hits),
     }
 
