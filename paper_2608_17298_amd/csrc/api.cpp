@@ -308,7 +308,7 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   uint32_t* perm = at<uint32_t>(f->scratch, L.perm);
   GART_HIP(iota_u32(perm, n, s));
   GART_HIP(radix_sort_u32(key, perm, at<uint32_t>(f->scratch, L.key_alt), at<uint32_t>(f->scratch, L.perm_alt), n,
-                          32, at<void>(f->scratch, L.radix_tmp), s));
+                          24, at<void>(f->scratch, L.radix_tmp), s));
   TileMapArgs T{};
   T.n = n;
   T.tile = settings->tile;

@@ -726,9 +726,15 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 // Chain rule: one Gaussian per lane of the first wave.  SH gradients: all
 // threads, coalesced.
 // ---------------------------------------------------------------------------
+#ifndef GART_REDUCE_BLOCK
+#define GART_REDUCE_BLOCK 256
+#endif
+#ifndef GART_REDUCE_GAUSSIANS
+#define GART_REDUCE_GAUSSIANS 64
+#endif
 constexpr int kReduceLanes = 16;
-constexpr int kReduceBlock = 256;
-constexpr int kReduceGaussians = 64;
+constexpr int kReduceBlock = GART_REDUCE_BLOCK;
+constexpr int kReduceGaussians = GART_REDUCE_GAUSSIANS;
 
 template <int K, bool ROWS>
 __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs A) {

@@ -103,7 +103,7 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
 
     double* G = A.geom + kGeomStride * i;
     int rx0 = 0, ry0 = 0, rx1 = -1, ry1 = -1;
-    float key = __int_as_float(0x7f800000);  // +inf: culled Gaussians sort last
+    uint32_t key = kDepthCodeCulled;  // culled Gaussians sort last
     if (ok) {
       const double inv = 1.0 / sqrt(qq);
       const double w = qw * inv, x = qx * inv, y = qy * inv, z = qz * inv;
@@ -178,8 +178,13 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
           lo = fmax(lo, sqrt(dist * dist - r * r) - ac * hb);
         }
         lo -= 1e-12 * (dist + r);
-        key = lo > 0.0 ? __double2float_rd(lo) : 0.0f;
-        G[kGeoKey] = double(key);
+        // The bound rounded down to a float whose low 8 mantissa bits are
+        // zero (relative step 2^-15): its bits shifted right by 8 are a
+        // 24-bit sort code (three 8-bit radix passes), and the value is still
+        // a lower bound.
+        const uint32_t kb = lo > 0.0 ? (__float_as_uint(__double2float_rd(lo)) & 0xffffff00u) : 0u;
+        key = kb >> 8;
+        G[kGeoKey] = double(__uint_as_float(kb));
         const int ts = A.tile;
         my_tiles = uint32_t(rx1 / ts - rx0 / ts + 1) * uint32_t(ry1 / ts - ry0 / ts + 1);
       } else {
@@ -192,7 +197,7 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
       for (int k = 0; k < kGeomStride; ++k) G[k] = 0.0;
       G[kGeoD2c] = -1.0;  // no ray can pass the hit test
       G[kGeoKey] = double(__int_as_float(0x7f800000));
-      key = __int_as_float(0x7f800000);
+      key = kDepthCodeCulled;
       rx0 = ry0 = 0;
       rx1 = ry1 = -1;
     }
@@ -202,7 +207,7 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
     A.rect[4 * i + 3] = ry1;
     A.area[i] = my_tiles ? int64_t(rx1 - rx0 + 1) * int64_t(ry1 - ry0 + 1) : 0;
     A.tile_count[i] = my_tiles;
-    A.depth_key[i] = __float_as_uint(key);
+    A.depth_key[i] = key;
     if (my_tiles) {
       // Colour bound over all directions: per band l, |sum_m sh_lm Y_lm| <=
       // |sh_l| sqrt((2l+1)/(4 pi)) (Cauchy-Schwarz and the addition theorem).

@@ -53,7 +53,7 @@ struct BoundsArgs {
   int64_t* area;            // [n] rectangle areas (scanned later into O_prim)
   double* geom;
   uint32_t* tile_count;
-  uint32_t* depth_key;      // [n] float bits of the depth lower bound
+  uint32_t* depth_key;      // [n] 24-bit code of the depth lower bound (kDepthCodeCulled if culled)
   // per block of kBoundsBlock Gaussians: [2b] sum of tile counts, [2b+1]
   // max colour bound (float bits); reduced by launch_bounds_totals
   unsigned long long* block_partial;
