@@ -39,6 +39,15 @@ def _scene(name):
         sc, _, _ = random_tiny_scene(np.random.default_rng(5), 300, 83, 61, 3, spread=1.0, ls_mu=-2.6,
                                      ls_sd=0.5, logit_mu=1.0)
         return sc
+    if name in ("random_sh1", "random_sh2"):  # the K = 4 and K = 9 kernel instantiations
+        deg = int(name[-1])
+        sc, _, _ = random_tiny_scene(np.random.default_rng(40 + deg), 400, 75, 58, deg, spread=1.0, ls_mu=-2.5,
+                                     ls_sd=0.5, logit_mu=0.5, high_sd=0.15)
+        return sc
+    if name == "random_sh3_tile16":  # 16x16 tiles (four pixel groups per tile) at SH degree 3
+        sc, _, _ = random_tiny_scene(np.random.default_rng(7), 500, 97, 70, 3, tile=16, spread=1.0, ls_mu=-2.4,
+                                     ls_sd=0.5, logit_mu=0.5)
+        return sc
     raise KeyError(name)
 
 
@@ -58,7 +67,8 @@ def _case(name, mode="gather", tile=None):
     return _cache[("scene", name)], o, info, ren, grads, _cache[key]
 
 
-SCENES = ["tiny", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3"]
+SCENES = ["tiny", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3", "random_sh1", "random_sh2",
+          "random_sh3_tile16"]
 
 
 @pytest.mark.parametrize("name", SCENES)
