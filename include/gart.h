@@ -23,6 +23,11 @@
  *    the sizes the caller declares.
  *  - One gart_frame is used by one stream at a time.  Calls on the same
  *    frame from different streams race.
+ *  - gart_build_tile_map, gart_forward, gart_backward and the training
+ *    calls only enqueue kernels (buffers are cleared by kernels, not by
+ *    memset), so they may be captured in a HIP graph and replayed while the
+ *    frame's sizes (N, pair count) stay the ones the capture saw.
+ *    gart_bounds synchronises the host and cannot be captured.
  *  - Scene: N Gaussians with mean mu, rotation from a quaternion q = (w, x,
  *    y, z) (any non-zero norm; normalised internally), per-axis scale
  *    s = exp(log_scale), opacity sigma = 1 / (1 + exp(-logit)) and RGB
