@@ -161,6 +161,9 @@ typedef struct {
   int64_t pair_capacity;  /* number of (tile, prim) pair slots allocated */
   uint32_t* pair_tile;    /* [pair_capacity] tile id of each pair, sorted ascending */
   uint32_t* pair_prim;    /* [pair_capacity] Gaussian index of each pair */
+  float* pair_key;        /* [pair_capacity] lower bound on tau (Eq. 3) of the Gaussian's maximum
+                             response along every pixel ray of the pair's tile; each tile's list is
+                             sorted ascending by it, then by Gaussian index */
   int64_t* tile_range;    /* [n_tiles+1] pairs of tile t are [tile_range[t], tile_range[t+1]) */
   /* written by gart_forward, read by gart_backward */
   int64_t lt_capacity;    /* number of intermediate entries allocated, each of
@@ -262,9 +265,11 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
 /* Tile-primitive mapping (Sec. 4.3 "reverse tile mapping").
  * Emits one (tile, Gaussian) pair per tile that a rectangle overlaps and
  * radix-sorts the pairs by tile id, then builds tile_range (the tile offset
- * table).  Within one tile, pairs are ordered by a conservative lower bound
- * on the depth at which the Gaussian can be hit (then by index); the set of
- * Gaussians per tile is exactly the set of rectangles meeting the tile.
+ * table).  Within one tile, pairs are ordered by pair_key, a conservative
+ * lower bound on the ray parameter at which the Gaussian can be hit by any
+ * pixel ray of that tile, kept to 24 bits or fewer of a log-scaled code and
+ * rounded down (then by index); the set of Gaussians per tile is exactly the
+ * set of rectangles meeting the tile.
  * Requires gart_bounds on the same frame first (else INVALID_ARG). */
 gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* settings, gart_frame* frame,
                                 void* stream);

@@ -39,8 +39,7 @@ gart_status fail(gart_status s, const char* fmt, ...) {
 size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t depth_key, key_alt, perm, perm_alt, base_rank, pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials,
-      acc, rows, row_flag, total;
+  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, acc, rows, row_flag, total;
 };
 
 Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
@@ -52,11 +51,6 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
     return o;
   };
   const int64_t nn = std::max<int64_t>(n, 1), pc = std::max<int64_t>(pair_cap, 1);
-  L.depth_key = take(nn * 4);
-  L.key_alt = take(nn * 4);
-  L.perm = take(nn * 4);
-  L.perm_alt = take(nn * 4);
-  L.base_rank = take((nn + 1) * 8);
   L.pair_key_alt = take(pc * 4);
   L.pair_val_alt = take(pc * 4);
   L.radix_tmp = take(radix_tmp_bytes(std::max(nn, pc)));
@@ -253,7 +247,6 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   A.area = f->lt_offset;
   A.geom = f->prim_geom;
   A.tile_count = f->tile_count;
-  A.depth_key = at<uint32_t>(f->scratch, L.depth_key);
   A.block_partial = at<unsigned long long>(f->scratch, L.partials);
   GART_HIP(launch_bounds(A, s));
   GART_HIP(scan_exclusive_i64(f->lt_offset, f->lt_offset, n, f->lt_offset + n, at<void>(f->scratch, L.scan_tmp), s));
@@ -298,41 +291,42 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   const int64_t n_tiles = int64_t(f->tiles_x) * f->tiles_y;
   GART_REQUIRE(f->pair_offset && f->tile_range, "frame pair_offset/tile_range is NULL");
   GART_REQUIRE(P <= f->pair_capacity, "pair capacity");
-  if (P > 0) GART_REQUIRE(f->pair_tile && f->pair_prim, "frame pair buffers are NULL");
+  if (P > 0) GART_REQUIRE(f->pair_tile && f->pair_prim && f->pair_key, "frame pair buffers are NULL");
   const int K = (f->sh_degree + 1) * (f->sh_degree + 1);
   const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  uint32_t* key = at<uint32_t>(f->scratch, L.depth_key);
-  uint32_t* perm = at<uint32_t>(f->scratch, L.perm);
-  GART_HIP(iota_u32(perm, n, s));
-  GART_HIP(radix_sort_u32(key, perm, at<uint32_t>(f->scratch, L.key_alt), at<uint32_t>(f->scratch, L.perm_alt), n,
-                          24, at<void>(f->scratch, L.radix_tmp), s));
   TileMapArgs T{};
   T.n = n;
   T.tile = settings->tile;
   T.tiles_x = f->tiles_x;
   T.tiles_y = f->tiles_y;
+  T.cam = make_cam(camera);
   T.rect = f->rect;
   T.tile_count = f->tile_count;
-  T.perm = perm;
-  T.base_rank = at<int64_t>(f->scratch, L.base_rank);
+  T.geom = f->prim_geom;
   T.pair_offset = f->pair_offset;
   T.keys = f->pair_tile;
   T.vals = f->pair_prim;
+  T.pair_key = f->pair_key;
   T.pair_count = P;
   T.tile_range = f->tile_range;
-  GART_HIP(launch_gather_counts(T, s));
-  GART_HIP(scan_exclusive_i64(T.base_rank, T.base_rank, n, T.base_rank + n, at<void>(f->scratch, L.scan_tmp), s));
-  GART_HIP(launch_scatter_pair_offset(T, s));
+  // Pair slots per Gaussian in index order, then one key per pair: tile id in
+  // the high bits, the pair's depth-bound code below; a stable sort by that
+  // key orders each tile's list by depth bound, then by Gaussian index.
+  int tile_bits = 1;
+  while ((int64_t(1) << tile_bits) < n_tiles) ++tile_bits;
+  T.key_bits = std::min(24, 32 - tile_bits);
+  GART_HIP(launch_pair_counts(T, s));
+  GART_HIP(scan_exclusive_i64(f->pair_offset, f->pair_offset, n, f->pair_offset + n, at<void>(f->scratch, L.scan_tmp), s));
   GART_HIP(launch_emit_pairs(T, s));
-  int bits = 1;
-  while ((int64_t(1) << bits) < n_tiles) ++bits;
   GART_HIP(record(f->events[GART_EV_SORT_BEGIN], s));
   GART_HIP(radix_sort_u32(f->pair_tile, f->pair_prim, at<uint32_t>(f->scratch, L.pair_key_alt),
-                          at<uint32_t>(f->scratch, L.pair_val_alt), P, bits, at<void>(f->scratch, L.radix_tmp), s));
+                          at<uint32_t>(f->scratch, L.pair_val_alt), P, tile_bits + T.key_bits,
+                          at<void>(f->scratch, L.radix_tmp), s));
   GART_HIP(record(f->events[GART_EV_SORT_END], s));
+  GART_HIP(launch_split_pair_keys(T, s));
   GART_HIP(launch_tile_ranges(f->pair_tile, P, n_tiles, f->tile_range, s));
   f->stage = 2;
   return GART_OK;
@@ -362,6 +356,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.t_min = settings->t_min;
   A.tile_range = f->tile_range;
   A.pair_prim = f->pair_prim;
+  A.pair_key = f->pair_key;
   A.geom = f->prim_geom;
   A.rect = f->rect;
   A.lt_offset = f->lt_offset;
@@ -414,6 +409,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.n = f->n;
   A.tile_range = f->tile_range;
   A.pair_prim = f->pair_prim;
+  A.pair_key = f->pair_key;
   A.geom = f->prim_geom;
   A.rect = f->rect;
   A.lt_offset = f->lt_offset;

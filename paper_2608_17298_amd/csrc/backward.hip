@@ -262,7 +262,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
   uint32_t nv = 0;
   for (int64_t j = beg + tid; j < end; j += NT) {
-    if (A.geom[int64_t(kGeomStride) * A.pair_prim[j] + kGeoKey] > tmax) break;
+    if (double(A.pair_key[j]) > tmax) break;
     ++nv;
   }
 #pragma unroll
@@ -660,7 +660,8 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
       const double* G = A.geom + int64_t(kGeomStride) * id;
       double* row = s_row + tid * kRow;
 #pragma unroll
-      for (int k = 0; k < 15; ++k) row[k] = G[k];
+      for (int k = 0; k < 14; ++k) row[k] = G[k];
+      row[14] = double(A.pair_key[base + tid]);
       row[15] = __longlong_as_double(A.lt_offset[id]);
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
       int* ri = reinterpret_cast<int*>(row + 16);

@@ -103,7 +103,7 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
 
     double* G = A.geom + kGeomStride * i;
     int rx0 = 0, ry0 = 0, rx1 = -1, ry1 = -1;
-    uint32_t key = kDepthCodeCulled;  // culled Gaussians sort last
+
     if (ok) {
       const double inv = 1.0 / sqrt(qq);
       const double w = qw * inv, x = qx * inv, y = qy * inv, z = qz * inv;
@@ -178,13 +178,7 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
           lo = fmax(lo, sqrt(dist * dist - r * r) - ac * hb);
         }
         lo -= 1e-12 * (dist + r);
-        // The bound rounded down to a float whose low 8 mantissa bits are
-        // zero (relative step 2^-15): its bits shifted right by 8 are a
-        // 24-bit sort code (three 8-bit radix passes), and the value is still
-        // a lower bound.
-        const uint32_t kb = lo > 0.0 ? (__float_as_uint(__double2float_rd(lo)) & 0xffffff00u) : 0u;
-        key = kb >> 8;
-        G[kGeoKey] = double(__uint_as_float(kb));
+        G[kGeoKey] = lo > 0.0 ? lo : 0.0;
         const int ts = A.tile;
         my_tiles = uint32_t(rx1 / ts - rx0 / ts + 1) * uint32_t(ry1 / ts - ry0 / ts + 1);
       } else {
@@ -197,7 +191,6 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
       for (int k = 0; k < kGeomStride; ++k) G[k] = 0.0;
       G[kGeoD2c] = -1.0;  // no ray can pass the hit test
       G[kGeoKey] = double(__int_as_float(0x7f800000));
-      key = kDepthCodeCulled;
       rx0 = ry0 = 0;
       rx1 = ry1 = -1;
     }
@@ -207,7 +200,6 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
     A.rect[4 * i + 3] = ry1;
     A.area[i] = my_tiles ? int64_t(rx1 - rx0 + 1) * int64_t(ry1 - ry0 + 1) : 0;
     A.tile_count[i] = my_tiles;
-    A.depth_key[i] = key;
     if (my_tiles) {
       // Colour bound over all directions: per band l, |sum_m sh_lm Y_lm| <=
       // |sh_l| sqrt((2l+1)/(4 pi)) (Cauchy-Schwarz and the addition theorem).
@@ -294,38 +286,76 @@ __global__ __launch_bounds__(256) void bounds_totals_kernel(const unsigned long 
   }
 }
 
-__global__ void gather_counts_kernel(TileMapArgs A) {
-  const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (r < A.n) A.base_rank[r] = A.tile_count[A.perm[r]];
+__global__ void pair_counts_kernel(TileMapArgs A) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < A.n) A.pair_offset[i] = A.tile_count[i];
 }
 
-__global__ void scatter_pair_offset_kernel(TileMapArgs A) {
-  const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (r < A.n) A.pair_offset[A.perm[r]] = A.base_rank[r];
-  if (r == 0) A.pair_offset[A.n] = A.base_rank[A.n];
+// Depth bound <-> `bits`-bit code, monotone over log2 depth in [-12, 20):
+// code 0 stands for 0 and depth_code_value(depth_code(x)) <= x.
+__device__ __forceinline__ double depth_code_value(uint32_t c, int bits) {
+  return c == 0 ? 0.0 : exp2(double(c) * (32.0 / double(1u << bits)) - 12.0);
+}
+__device__ __forceinline__ uint32_t depth_code(double x, int bits) {
+  if (!(x > 0x1p-12)) return 0u;
+  const double q = fmin(fmax(floor((log2(x) + 12.0) * (double(1u << bits) / 32.0)), 1.0), double((1u << bits) - 1));
+  uint32_t c = uint32_t(q);
+  while (c > 0 && depth_code_value(c, bits) > x) --c;  // rounding of log2 / exp2
+  return c;
 }
 
-// One block emits the pairs of 256 consecutive depth ranks; its threads
-// stride over the block's pair slots and find their rank by binary search
-// over the ranks' first slots held in LDS.
-constexpr int kEmitRanks = 256;
+// One block emits the pairs of 256 consecutive Gaussians (index order); its
+// threads stride over the block's pair slots and find their Gaussian by
+// binary search over first slots held in LDS.  Each pair gets a lower bound
+// on the depth tau of any hit of its Gaussian in its tile: the larger of the
+// Gaussian's own bound and a bound over the tile's pixel rays.  With the
+// unnormalised ray d = R^T (a, b, 1), a = (x + 1/2 - cx)/fx, b = (y + 1/2 -
+// cy)/fy, the max-response depth is tau = N |d| / D with N = n . (a, b, 1)
+// (linear), D = (a, b, 1) M (a, b, 1)^T (convex), |d| = sqrt(a^2 + b^2 + 1),
+// n = R Sigma^-1 (mu - o) and M = R Sigma^-1 R^T (R = world -> camera).  Over
+// the tile's rectangle of (a, b), N is smallest and D largest at corners and
+// |d| smallest at the point nearest (0, 0); a hit needs tau > 0, so
+// tau >= max(N_min, 0) |d|_min / D_max.
+constexpr int kEmitGaussians = 256;
 
 __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
-  __shared__ int64_t s_base[kEmitRanks + 1];
-  __shared__ int32_t s_rect[kEmitRanks][4];
-  __shared__ uint32_t s_prim[kEmitRanks];
-  const int64_t r0 = int64_t(blockIdx.x) * kEmitRanks;
-  const int nr = int(std::min<int64_t>(kEmitRanks, A.n - r0));
-  for (int k = threadIdx.x; k <= nr; k += blockDim.x) s_base[k] = A.base_rank[r0 + k];
+  __shared__ int64_t s_base[kEmitGaussians + 1];
+  __shared__ int32_t s_rect[kEmitGaussians][4];
+  __shared__ double s_q[kEmitGaussians][10];  // M (m00 m01 m02 m11 m12 m22), n (3), the Gaussian's bound
+  const int64_t i0 = int64_t(blockIdx.x) * kEmitGaussians;
+  const int nr = int(std::min<int64_t>(kEmitGaussians, A.n - i0));
+  for (int k = threadIdx.x; k <= nr; k += blockDim.x) s_base[k] = A.pair_offset[i0 + k];
   for (int k = threadIdx.x; k < nr; k += blockDim.x) {
-    const uint32_t p = A.perm[r0 + k];
-    s_prim[k] = p;
+    const int64_t i = i0 + k;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) s_rect[k][c] = A.rect[4 * int64_t(p) + c];
+    for (int c = 0; c < 4; ++c) s_rect[k][c] = A.rect[4 * i + c];
+    if (A.tile_count[i] == 0) continue;
+    const double* G = A.geom + int64_t(kGeomStride) * i;
+    // P = W Rt maps (a, b, 1) to d_g = W d (Rt: camera -> world)
+    double P[9];
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+      for (int c = 0; c < 3; ++c)
+        P[3 * r + c] = fma(G[kGeoW + 3 * r], A.cam.Rt[c],
+                           fma(G[kGeoW + 3 * r + 1], A.cam.Rt[3 + c], G[kGeoW + 3 * r + 2] * A.cam.Rt[6 + c]));
+    auto m = [&](int a, int b) { return fma(P[a], P[b], fma(P[3 + a], P[3 + b], P[6 + a] * P[6 + b])); };
+    s_q[k][0] = m(0, 0);
+    s_q[k][1] = m(0, 1);
+    s_q[k][2] = m(0, 2);
+    s_q[k][3] = m(1, 1);
+    s_q[k][4] = m(1, 2);
+    s_q[k][5] = m(2, 2);
+    // n = P^T W (mu - o) = -P^T o_g
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+      s_q[k][6 + a] = -fma(P[a], G[kGeoOg], fma(P[3 + a], G[kGeoOg + 1], P[6 + a] * G[kGeoOg + 2]));
+    s_q[k][9] = G[kGeoKey];
   }
   __syncthreads();
   const int64_t first = s_base[0], last = s_base[nr];
   const int ts = A.tile;
+  const double ifx = 1.0 / A.cam.fx, ify = 1.0 / A.cam.fy;
   for (int64_t j = first + threadIdx.x; j < last; j += blockDim.x) {
     int lo = 0, hi = nr - 1;  // largest k with s_base[k] <= j
     while (lo < hi) {
@@ -337,9 +367,36 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
     const int tx0 = s_rect[k][0] / ts, ty0 = s_rect[k][1] / ts, tx1 = s_rect[k][2] / ts;
     const int ntx = tx1 - tx0 + 1;
     const int tx = tx0 + int(q % ntx), ty = ty0 + int(q / ntx);
-    A.keys[j] = uint32_t(ty) * uint32_t(A.tiles_x) + uint32_t(tx);
-    A.vals[j] = s_prim[k];
+    // the tile's pixel-centre rectangle in (a, b)
+    const double a0 = (double(tx * ts) + 0.5 - A.cam.cx) * ifx;
+    const double a1 = (double(min(A.cam.W - 1, tx * ts + ts - 1)) + 0.5 - A.cam.cx) * ifx;
+    const double b0 = (double(ty * ts) + 0.5 - A.cam.cy) * ify;
+    const double b1 = (double(min(A.cam.H - 1, ty * ts + ts - 1)) + 0.5 - A.cam.cy) * ify;
+    const double* Q = s_q[k];
+    double nmin = __builtin_huge_val(), dmax = 0.0;
+#pragma unroll
+    for (int corner = 0; corner < 4; ++corner) {
+      const double a = (corner & 1) ? a1 : a0, b = (corner & 2) ? b1 : b0;
+      nmin = fmin(nmin, fma(Q[6], a, fma(Q[7], b, Q[8])));
+      const double D = fma(a, fma(Q[0], a, 2.0 * fma(Q[1], b, Q[2])), fma(b, fma(Q[3], b, 2.0 * Q[4]), Q[5]));
+      dmax = fmax(dmax, D);
+    }
+    const double am = (a0 <= 0.0 && a1 >= 0.0) ? 0.0 : fmin(fabs(a0), fabs(a1));
+    const double bm = (b0 <= 0.0 && b1 >= 0.0) ? 0.0 : fmin(fabs(b0), fabs(b1));
+    double tk = nmin > 0.0 ? nmin * sqrt(fma(am, am, fma(bm, bm, 1.0))) / dmax : 0.0;
+    tk -= 1e-12 * tk;  // rounding of the bound's fp64 evaluation
+    const double bound = fmax(Q[9], tk);
+    A.keys[j] = (uint32_t(ty * A.tiles_x + tx) << A.key_bits) | depth_code(bound, A.key_bits);
+    A.vals[j] = uint32_t(i0 + k);
   }
+}
+
+__global__ void split_pair_keys_kernel(TileMapArgs A) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= A.pair_count) return;
+  const uint32_t key = A.keys[j];
+  A.keys[j] = key >> A.key_bits;
+  A.pair_key[j] = __double2float_rd(depth_code_value(key & ((1u << A.key_bits) - 1u), A.key_bits));
 }
 
 // tile_range[t] = first sorted pair whose tile id is >= t.
@@ -373,20 +430,21 @@ hipError_t launch_bounds_totals(const unsigned long long* block_partial, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_gather_counts(const TileMapArgs& a, hipStream_t s) {
+hipError_t launch_pair_counts(const TileMapArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  gather_counts_kernel<<<ceil_div(a.n, 256), 256, 0, s>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_scatter_pair_offset(const TileMapArgs& a, hipStream_t s) {
-  scatter_pair_offset_kernel<<<std::max<int64_t>(1, ceil_div(a.n, 256)), 256, 0, s>>>(a);
+  pair_counts_kernel<<<ceil_div(a.n, 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.pair_count <= 0) return hipSuccess;
-  emit_pairs_kernel<<<ceil_div(a.n, kEmitRanks), 256, 0, s>>>(a);
+  emit_pairs_kernel<<<ceil_div(a.n, kEmitGaussians), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_split_pair_keys(const TileMapArgs& a, hipStream_t s) {
+  if (a.pair_count <= 0) return hipSuccess;
+  split_pair_keys_kernel<<<ceil_div(a.pair_count, 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -22,7 +22,6 @@ constexpr int kGeomStride = 16;  // doubles per Gaussian in prim_geom
 constexpr int kGeoW = 0, kGeoOg = 9, kGeoD2c = 12, kGeoSigma = 13, kGeoKey = 14;
 
 constexpr uint32_t kNoPrim = 0xffffffffu;
-constexpr uint32_t kDepthCodeCulled = 0x7f8000u;  // depth code of a culled Gaussian: +inf bits >> 8 (sorts last)
 
 // Camera constants, computed on the host in double from the float inputs.
 struct CamParams {

@@ -86,6 +86,10 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   double e_tau = kInf;  // smallest dropped hit (all buffered hits are smaller)
   uint32_t e_id = kNoPrim;
   uint32_t jr = UINT_MAX;  // first list position holding a dropped hit
+  // A rescan starts the wave at the smallest jr of its lanes; a lane skips
+  // the positions before its own jr (from): every hit there was composited
+  // in an earlier pass.
+  uint32_t from = 0;
 #pragma unroll
   for (int s = 0; s < KB; ++s) {
     bt[s] = kInf;
@@ -186,19 +190,18 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
         ri[2] = r.z;
         ri[3] = r.w;
         reinterpret_cast<uint32_t*>(row + 18)[0] = id;
-        s_key[tid] = float(G[kGeoKey]);
+        s_key[tid] = A.pair_key[base + tid];
       }
       if (tid == 0) {
         const int64_t nx = base + nb;
-        s_key[nb] = (nx < end) ? float(A.geom[int64_t(kGeomStride) * A.pair_prim[nx] + kGeoKey])
-                               : __int_as_float(0x7f800000);
+        s_key[nb] = (nx < end) ? A.pair_key[nx] : __int_as_float(0x7f800000);
       }
       __syncthreads();
       if (!done && !finished && !stalled) {
         for (int c = 0; c < nb; ++c) {
           const double* row = s_row + c * kRow;
           const int4 r = *reinterpret_cast<const int4*>(row + 16);
-          if (px >= r.x && px <= r.z && py >= r.y && py <= r.w) {
+          if (uint32_t(base - beg) + uint32_t(c) >= from && px >= r.x && px <= r.z && py >= r.y && py <= r.w) {
             ++n_tests;
             double W[9], og[3];
 #pragma unroll
@@ -283,6 +286,7 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
     restart = rs;
     ++passes;
     if (need) {
+      from = jr;
       e_tau = kInf;
       e_id = kNoPrim;
       jr = UINT_MAX;

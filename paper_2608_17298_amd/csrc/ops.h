@@ -53,7 +53,6 @@ struct BoundsArgs {
   int64_t* area;            // [n] rectangle areas (scanned later into O_prim)
   double* geom;
   uint32_t* tile_count;
-  uint32_t* depth_key;      // [n] 24-bit code of the depth lower bound (kDepthCodeCulled if culled)
   // per block of kBoundsBlock Gaussians: [2b] sum of tile counts, [2b+1]
   // max colour bound (float bits); reduced by launch_bounds_totals
   unsigned long long* block_partial;
@@ -68,19 +67,22 @@ hipError_t launch_bounds_totals(const unsigned long long* block_partial, int64_t
 struct TileMapArgs {
   int64_t n;
   int32_t tile, tiles_x, tiles_y;
+  CamParams cam;
   const int32_t* rect;
   const uint32_t* tile_count;
-  const uint32_t* perm;     // [n] Gaussian index at each depth rank
-  int64_t* base_rank;       // [n+1] scratch: first pair slot per rank (scanned in place)
-  int64_t* pair_offset;     // [n+1] output: first pair slot per Gaussian index
-  uint32_t* keys;           // [P] emitted tile ids
+  const double* geom;       // [n, 16] per-Gaussian geometry (W, o_g, per-Gaussian depth bound)
+  int64_t* pair_offset;     // [n+1] first pair slot of each Gaussian (tile counts, scanned in place)
+  uint32_t* keys;           // [P] (tile << key_bits) | depth code of each emitted pair
   uint32_t* vals;           // [P] emitted Gaussian indices
+  float* pair_key;          // [P] depth bound of each sorted pair (decoded code)
+  int32_t key_bits;         // bits of the depth code in keys
   int64_t pair_count;
   int64_t* tile_range;      // [n_tiles+1]
 };
-hipError_t launch_gather_counts(const TileMapArgs& a, hipStream_t s);
-hipError_t launch_scatter_pair_offset(const TileMapArgs& a, hipStream_t s);
+hipError_t launch_pair_counts(const TileMapArgs& a, hipStream_t s);
 hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s);
+// keys -> tile ids in place, and the decoded depth bound of each pair
+hipError_t launch_split_pair_keys(const TileMapArgs& a, hipStream_t s);
 hipError_t launch_tile_ranges(const uint32_t* sorted_keys, int64_t pair_count, int64_t n_tiles, int64_t* tile_range,
                               hipStream_t s);
 
@@ -91,6 +93,7 @@ struct ForwardArgs {
   double t_min;
   const int64_t* tile_range;
   const uint32_t* pair_prim;
+  const float* pair_key;     // [pairs] depth lower bound of each pair (ascending in a tile list)
   const double* geom;
   const int32_t* rect;
   const int64_t* lt_offset;
@@ -114,6 +117,7 @@ struct BackwardArgs {
   int64_t n;
   const int64_t* tile_range;
   const uint32_t* pair_prim;
+  const float* pair_key;     // [pairs] depth lower bound of each pair (ascending in a tile list)
   const double* geom;
   const int32_t* rect;
   const int64_t* lt_offset;

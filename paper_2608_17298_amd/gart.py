@@ -71,7 +71,7 @@ class gart_settings(ctypes.Structure):
 class gart_frame(ctypes.Structure):
     _fields_ = [("rect", _P), ("lt_offset", _P), ("prim_geom", _P), ("tile_count", _P),
                 ("pair_offset", _P), ("pair_capacity", ctypes.c_int64), ("pair_tile", _P), ("pair_prim", _P),
-                ("tile_range", _P), ("lt_capacity", ctypes.c_int64), ("lt", _P), ("pixel_state", _P), ("hit_list", _P),
+                ("pair_key", _P), ("tile_range", _P), ("lt_capacity", ctypes.c_int64), ("lt", _P), ("pixel_state", _P), ("hit_list", _P),
                 ("scratch", _P), ("scratch_bytes", ctypes.c_size_t), ("counters", _P),
                 ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
@@ -250,7 +250,7 @@ class Frame:
         self.counters = torch.zeros(NUM_COUNTERS, dtype=torch.int64, **dev) if counters else None
         self.c = gart_frame()
         self.events = [None] * NUM_EVENTS
-        self.lt = self.pair_tile = self.pair_prim = self.scratch = None
+        self.lt = self.pair_tile = self.pair_prim = self.pair_key = self.scratch = None
         self._alloc_lt(lt_capacity)
         self._alloc_pairs(pair_capacity)
 
@@ -266,6 +266,7 @@ class Frame:
         cap = int(cap)
         self.pair_tile = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
         self.pair_prim = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
+        self.pair_key = torch.empty(max(cap, 1), dtype=torch.float32, device=self.device)
         # composited-hit lists: tile^2 slots per pair (see gart_frame.hit_list)
         self.hit_list = torch.empty(max(cap, 1) * self.settings.tile ** 2, dtype=torch.int32, device=self.device)
         self.pair_capacity = cap
@@ -282,7 +283,7 @@ class Frame:
             self.lt = None
             self._alloc_lt(int(lt_entries * slack) + 1)
         if pair_count > self.pair_capacity:
-            self.pair_tile = self.pair_prim = self.hit_list = self.scratch = None
+            self.pair_tile = self.pair_prim = self.pair_key = self.hit_list = self.scratch = None
             self._alloc_pairs(int(pair_count * slack) + 1)
 
     def c_struct(self) -> gart_frame:
@@ -291,6 +292,7 @@ class Frame:
         f.tile_count, f.pair_offset = _ptr(self.tile_count), _ptr(self.pair_offset)
         f.pair_capacity = self.pair_capacity
         f.pair_tile, f.pair_prim, f.tile_range = _ptr(self.pair_tile), _ptr(self.pair_prim), _ptr(self.tile_range)
+        f.pair_key = _ptr(self.pair_key)
         f.lt_capacity = self.lt_capacity
         f.lt, f.pixel_state, f.hit_list = _ptr(self.lt), _ptr(self.pixel_state), _ptr(self.hit_list)
         f.scratch, f.scratch_bytes = _ptr(self.scratch), self.scratch.numel()

@@ -83,6 +83,7 @@ def run_gpu(scene, mode="gather", tile=None, dl=None, counters=True, keep_frame=
         tile_count=frame.tile_count.cpu().numpy()[:n].view(np.uint32), geom=frame.prim_geom.cpu().numpy()[:n],
         pair_tile=frame.pair_tile.cpu().numpy()[:P].view(np.uint32),
         pair_prim=frame.pair_prim.cpu().numpy()[:P].view(np.uint32),
+        pair_key=frame.pair_key.cpu().numpy()[:P],
         pair_offset=frame.pair_offset.cpu().numpy()[:n + 1], tile_range=frame.tile_range.cpu().numpy(),
         image=image.cpu().numpy(), tau_end=ps["tau_end"], id_end=ps["id_end"].astype(np.int64),
         n_hits=ps["n_hits"].astype(np.int64), state_color=ps["color"], t_final=ps["t_final"],

@@ -87,12 +87,12 @@ def test_tile_lists_bit_exact(name):
     off, prim = oracle.tile_lists(info.rect, info.state, o.W, o.H, ts)
     assert np.array_equal(gpu["tile_range"], off)
     assert gpu["pair_count"] == len(prim)
-    key = gpu["geom"][:, 14]
+    key = gpu["pair_key"]
     gp = gpu["pair_prim"].astype(np.int64)
     for t in range(len(off) - 1):
         seg = gp[off[t]:off[t + 1]]
         assert np.array_equal(np.sort(seg), prim[off[t]:off[t + 1]]), t
-        k = key[seg]
+        k = key[off[t]:off[t + 1]]
         # front-to-back order inside a tile: depth lower bound, then index
         assert np.all((np.diff(k) > 0) | ((np.diff(k) == 0) & (np.diff(seg) > 0))), t
     assert np.all(gpu["pair_tile"][:-1] <= gpu["pair_tile"][1:])
@@ -101,6 +101,38 @@ def test_tile_lists_bit_exact(name):
     po = gpu["pair_offset"]
     order = act[np.argsort(po[act], kind="stable")]
     assert np.array_equal(np.diff(np.append(po[order], po[-1])), gpu["tile_count"][order].astype(np.int64))
+
+
+@pytest.mark.parametrize("name", ["small_reduced", "1m_reduced", "stress_reduced", "random_sh3_tile16"])
+def test_pair_keys_bound_every_hit(name):
+    """Each pair's key is at most the oracle's tau (Eq. 3) at every pixel of
+    its tile where the ray hits the Gaussian: the forward's early compositing
+    and the backward's list cut-off rely on it."""
+    sc, o, info, ren, grads, gpu = _case(name)
+    ts, W = sc.tile, o.W
+    tx_n = (W + ts - 1) // ts
+    rng = np.random.default_rng(7)
+    P = gpu["pair_count"]
+    sel = rng.choice(P, min(P, 4000), replace=False)
+    pix, prims, keys = [], [], []
+    for j in sel:
+        t, i = int(gpu["pair_tile"][j]), int(gpu["pair_prim"][j])
+        x0, y0, x1, y1 = info.rect[i]
+        tx, ty = t % tx_n, t // tx_n
+        xs = np.arange(max(x0, tx * ts), min(x1, tx * ts + ts - 1) + 1)
+        ys = np.arange(max(y0, ty * ts), min(y1, ty * ts + ts - 1) + 1)
+        assert len(xs) > 0 and len(ys) > 0, (j, t, i)
+        p = (ys[:, None] * W + xs[None, :]).ravel()
+        pix.append(p)
+        prims.append(np.full(p.size, i))
+        keys.append(np.full(p.size, gpu["pair_key"][j], np.float64))
+    pix, prims, keys = np.concatenate(pix), np.concatenate(prims), np.concatenate(keys)
+    r = o.ray_prim(pix, prims)
+    hit = r["hit"]
+    assert hit.any()
+    assert np.all(keys[hit] <= r["tau"][hit]), np.max(keys[hit] - r["tau"][hit])
+    # the per-tile bound is not vacuous: most hit pairs get a positive key
+    assert np.mean(keys[hit] > 0) > 0.5
 
 
 @pytest.mark.parametrize("name", SCENES)
