@@ -267,9 +267,10 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
  * radix-sorts the pairs by tile id, then builds tile_range (the tile offset
  * table).  Within one tile, pairs are ordered by pair_key, a conservative
  * lower bound on the ray parameter at which the Gaussian can be hit by any
- * pixel ray of that tile, kept to 24 bits or fewer of a log-scaled code and
- * rounded down (then by index); the set of Gaussians per tile is exactly the
- * set of rectangles meeting the tile.
+ * pixel ray of that tile, rounded down to a float with min(24, 32 - tile id
+ * bits) - 5 mantissa bits (0 below 2^-12, saturating below 2^20), then by
+ * index; the set of Gaussians per tile is exactly the set of rectangles
+ * meeting the tile.
  * Requires gart_bounds on the same frame first (else INVALID_ARG). */
 gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* settings, gart_frame* frame,
                                 void* stream);

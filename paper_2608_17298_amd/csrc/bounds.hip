@@ -291,17 +291,25 @@ __global__ void pair_counts_kernel(TileMapArgs A) {
   if (i < A.n) A.pair_offset[i] = A.tile_count[i];
 }
 
-// Depth bound <-> `bits`-bit code, monotone over log2 depth in [-12, 20):
-// code 0 stands for 0 and depth_code_value(depth_code(x)) <= x.
-__device__ __forceinline__ double depth_code_value(uint32_t c, int bits) {
-  return c == 0 ? 0.0 : exp2(double(c) * (32.0 / double(1u << bits)) - 12.0);
-}
+// Depth bound <-> `bits`-bit code: the float at or below the bound, cut to
+// the 32 binary exponents of [2^-12, 2^20) (5 bits) and the leading
+// bits - 5 mantissa bits.  The code is monotone in the bound (the bits of a
+// positive float are), saturates above 2^20, is 0 below 2^-12 and for fewer
+// than 6 bits, and its value (code 0 stands for 0) never exceeds the bound.
 __device__ __forceinline__ uint32_t depth_code(double x, int bits) {
-  if (!(x > 0x1p-12)) return 0u;
-  const double q = fmin(fmax(floor((log2(x) + 12.0) * (double(1u << bits) / 32.0)), 1.0), double((1u << bits) - 1));
-  uint32_t c = uint32_t(q);
-  while (c > 0 && depth_code_value(c, bits) > x) --c;  // rounding of log2 / exp2
-  return c;
+  if (bits < 6) return 0u;
+  const float f = __double2float_rd(x);
+  if (!(f >= 0x1p-12f)) return 0u;
+  const int m = bits - 5;
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t e = (u >> 23) - (127u - 12u);
+  if (e >= 32u) return (1u << bits) - 1u;
+  return (e << m) | ((u & 0x7fffffu) >> (23 - m));
+}
+__device__ __forceinline__ float depth_code_value(uint32_t c, int bits) {
+  if (c == 0 || bits < 6) return 0.0f;
+  const int m = bits - 5;
+  return __uint_as_float((((c >> m) + 127u - 12u) << 23) | ((c & ((1u << m) - 1u)) << (23 - m)));
 }
 
 // One block emits the pairs of 256 consecutive Gaussians (index order); its
@@ -396,7 +404,7 @@ __global__ void split_pair_keys_kernel(TileMapArgs A) {
   if (j >= A.pair_count) return;
   const uint32_t key = A.keys[j];
   A.keys[j] = key >> A.key_bits;
-  A.pair_key[j] = __double2float_rd(depth_code_value(key & ((1u << A.key_bits) - 1u), A.key_bits));
+  A.pair_key[j] = depth_code_value(key & ((1u << A.key_bits) - 1u), A.key_bits);
 }
 
 // tile_range[t] = first sorted pair whose tile id is >= t.

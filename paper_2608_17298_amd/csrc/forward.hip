@@ -21,10 +21,19 @@ namespace gart {
 namespace {
 
 #ifndef GART_FWD_KB
-#define GART_FWD_KB 16
+#define GART_FWD_KB 14
 #endif
 #ifndef GART_FWD_FLUSH
 #define GART_FWD_FLUSH 16
+#endif
+#ifndef GART_FWD_BATCH
+#define GART_FWD_BATCH 256
+#endif
+// Minimum waves per SIMD asked of the register allocator (default: none).
+#ifdef GART_FWD_WAVES
+#define GART_FWD_LAUNCH_BOUNDS(n) __launch_bounds__(n, GART_FWD_WAVES)
+#else
+#define GART_FWD_LAUNCH_BOUNDS(n) __launch_bounds__(n)
 #endif
 
 constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
@@ -36,16 +45,17 @@ constexpr int kMaxPasses = 1 << 20;
 // [15] O_prim (int64 bits), [16..17] rect (4 x int32), [18] index (uint32)
 
 template <int TILE, int K, int FMT>
-__global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
+__global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int NT = TILE * TILE;
   constexpr int KB = GART_FWD_KB;  // per-lane hit buffer (registers)
   constexpr int kFlushEvery = GART_FWD_FLUSH;
+  constexpr int NB = GART_FWD_BATCH < NT ? GART_FWD_BATCH : NT;  // candidates staged per batch
   constexpr double kInf = __builtin_huge_val();
 
   constexpr int KP = (K + 3) & ~3;  // SH basis row padded to 16 bytes
-  __shared__ __align__(16) double s_row[NT * kRow];
+  __shared__ __align__(16) double s_row[NB * kRow];
   __shared__ __align__(16) float s_Y[NT][KP];  // SH basis of each pixel's ray
-  __shared__ float s_key[NT + 1];
+  __shared__ float s_key[NB + 1];
   __shared__ unsigned s_restart;
 
   const int n_tiles = A.tiles_x * A.tiles_y;
@@ -174,8 +184,8 @@ __global__ __launch_bounds__(TILE* TILE) void forward_kernel(ForwardArgs A) {
   uint32_t restart = 0;
   int passes = 0;
   for (;;) {
-    for (int64_t base = beg + restart; base < end; base += NT) {
-      const int nb = int(min<int64_t>(NT, end - base));
+    for (int64_t base = beg + restart; base < end; base += NB) {
+      const int nb = int(min<int64_t>(NB, end - base));
       if (tid < nb) {
         const uint32_t id = A.pair_prim[base + tid];
         const double* G = A.geom + int64_t(kGeomStride) * id;

@@ -17,7 +17,10 @@ constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;
 
 constexpr int kSortThreads = 256;
-constexpr int kSortItems = 16;
+#ifndef GART_SORT_ITEMS
+#define GART_SORT_ITEMS 16
+#endif
+constexpr int kSortItems = GART_SORT_ITEMS;  // keys per thread and radix pass
 constexpr int kSortTile = kSortThreads * kSortItems;
 constexpr int kWaves = kSortThreads / 64;
 
