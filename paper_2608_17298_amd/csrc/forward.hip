@@ -178,6 +178,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
       bc[s] = bc[s + 1];
       bid[s] = bid[s + 1];
     }
+    bt[KB - 1] = kInf;  // unused slots hold depth +inf
     --cnt;
   };
 
@@ -237,26 +238,35 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
                 }
                 if (ins) {
                   const double a = row[13] * exp(-0.5 * D2);
+                  // Position = entries with a smaller (depth, index) key.
+                  // Unused slots hold depth +inf, so a strict depth count
+                  // needs no occupancy test; equal depths (rare) also count
+                  // the entries of smaller index.  Shift and placement are
+                  // selects, not branches.
                   int pos = 0;
-#pragma unroll
-                  for (int s = 0; s < KB; ++s) pos += (s < cnt && key_less(bt[s], bid[s], tau, id)) ? 1 : 0;
-#pragma unroll
-                  for (int s = KB - 1; s >= 1; --s) {
-                    if (s > pos && s <= cnt) {
-                      bt[s] = bt[s - 1];
-                      ba[s] = ba[s - 1];
-                      bc[s] = bc[s - 1];
-                      bid[s] = bid[s - 1];
-                    }
-                  }
+                  bool tie = false;
 #pragma unroll
                   for (int s = 0; s < KB; ++s) {
-                    if (s == pos) {
-                      bt[s] = tau;
-                      ba[s] = a;
-                      bc[s] = cpos;
-                      bid[s] = id;
-                    }
+                    pos += bt[s] < tau ? 1 : 0;
+                    tie = tie || bt[s] == tau;
+                  }
+                  if (tie) {
+#pragma unroll
+                    for (int s = 0; s < KB; ++s) pos += (bt[s] == tau && bid[s] < id) ? 1 : 0;
+                  }
+#pragma unroll
+                  for (int s = KB - 1; s >= 1; --s) {
+                    const bool sh = s > pos, pl = s == pos;
+                    bt[s] = sh ? bt[s - 1] : (pl ? tau : bt[s]);
+                    ba[s] = sh ? ba[s - 1] : (pl ? a : ba[s]);
+                    bc[s] = sh ? bc[s - 1] : (pl ? cpos : bc[s]);
+                    bid[s] = sh ? bid[s - 1] : (pl ? id : bid[s]);
+                  }
+                  if (pos == 0) {
+                    bt[0] = tau;
+                    ba[0] = a;
+                    bc[0] = cpos;
+                    bid[0] = id;
                   }
                   ++cnt;
                 }
