@@ -134,8 +134,10 @@ __device__ __forceinline__ float wave_sum32_transposed(float* v) {
 //     atomics).  Units without a composited hit are dropped, the rest are
 //     dealt to lanes in order of hit count, so the lanes of a round run
 //     loops of similar length.
-//  3. Each lane accumulates the gradient of one unit's hits in registers and
-//     writes one partial row (or adds it atomically).
+//  3. Each lane accumulates the gradient of one unit's hits in registers
+//     (a unit with more than kSplit hits is shared by two lanes, whose sums
+//     are then added across lanes) and writes one partial row (or adds it
+//     atomically).
 // ---------------------------------------------------------------------------
 constexpr int kUnits = 512;  // units per LDS pass
 constexpr int kBatch = 8;    // composited hits whose (L,T) loads are issued together
@@ -144,20 +146,18 @@ constexpr int kBatch = 8;    // composited hits whose (L,T) loads are issued tog
 #endif
 constexpr int kWaveMin = GART_WAVE_MIN;  // hits from which a unit is evaluated by its whole wave (mode GATHER_WAVE)
 
-// Lane groups: a unit with more than kSplit4 composited hits is shared by 4
-// adjacent lanes, one with more than kSplit2 by 2.  Lane j of a group of s
-// takes the unit's hits of rank j mod s (ranks in row-major pixel order), and
-// the group's partial sums are added across its lanes before its first lane
-// writes the row.  A round's time is its largest per-lane hit count, so
-// sharing the largest units evens the lanes of a round.
-#ifndef GART_SPLIT2
-#define GART_SPLIT2 8
+// Lane pairs: a unit with more than kSplit composited hits is shared by two
+// adjacent lanes.  Lane j of the pair takes the unit's hits of rank j mod 2
+// (ranks in row-major pixel order), and the pair's partial sums are added
+// across the two lanes before the first writes the row.  A round's time is
+// its largest per-lane hit count, so sharing the largest units evens the
+// lanes of a round.  (Groups of four lanes above 16 hits were slower: the
+// second cross-lane sum cost more than the shorter rounds saved.)
+#ifndef GART_SPLIT
+#define GART_SPLIT 6
 #endif
-#ifndef GART_SPLIT4
-#define GART_SPLIT4 16
-#endif
-constexpr int kSplit2 = GART_SPLIT2, kSplit4 = GART_SPLIT4;
-static_assert(0 < kSplit2 && kSplit2 <= kSplit4 && kSplit4 < 64, "split thresholds");
+constexpr int kSplit = GART_SPLIT;
+static_assert(0 < kSplit && kSplit < 64, "split threshold");
 
 // Inclusive prefix parity: bit b of the result is the parity of bits 0..b of x.
 __device__ __forceinline__ uint64_t prefix_parity(uint64_t x) {
@@ -170,21 +170,16 @@ __device__ __forceinline__ uint64_t prefix_parity(uint64_t x) {
   return x;
 }
 
-// The set bits of m whose rank (0 = lowest set bit) is j mod s, s in {1, 2, 4}.
-__device__ __forceinline__ uint64_t rank_subset(uint64_t m, int s, int j) {
-  if (s == 1) return m;
+// The set bits of m whose rank (0 = lowest set bit) is even (j = 0) or odd.
+__device__ __forceinline__ uint64_t rank_half(uint64_t m, int j) {
   const uint64_t p = prefix_parity(m);  // 1 at even ranks
-  const uint64_t h = (j & 1) ? (m & ~p) : (m & p);
-  if (s == 2) return h;
-  const uint64_t q = prefix_parity(h);
-  return (j & 2) ? (h & ~q) : (h & q);
+  return j ? (m & ~p) : (m & p);
 }
 
-// Value of the lane whose index differs in bit 0 (CTRL 0xb1) or bit 1 (0x4e):
-// DPP quad permutations, which need every lane of the wave active.
-template <int CTRL>
-__device__ __forceinline__ float quad_swap(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+// Value of the lane whose index differs in bit 0 (a DPP quad permutation,
+// which needs every lane of the wave active).
+__device__ __forceinline__ float pair_swap(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xb1, 0xf, 0xf, false));
 }
 
 // Per-pixel ray direction in LDS, padded to 32 bytes.
@@ -214,10 +209,9 @@ __device__ __forceinline__ int deal_units(int nu, const uint8_t* s_bucket, uint3
     // bucket b holds the units with 64 - b hits: those with >= dense_min
     // hits are buckets 0 .. 64 - dense_min, the first entries of the order
     if (s_dense && int(threadIdx.x) == 64 - dense_min) *s_dense = inc;
-    // units with more than kSplit4 (kSplit2) hits: buckets below 64 - kSplit4
-    // (64 - kSplit2), the first entries of the order
-    if (s_split && threadIdx.x == 64 - kSplit4) s_split[0] = inc - c;
-    if (s_split && threadIdx.x == 64 - kSplit2) s_split[1] = inc - c;
+    // units with more than kSplit hits: buckets below 64 - kSplit, the first
+    // entries of the order
+    if (s_split && threadIdx.x == 64 - kSplit) *s_split = inc - c;
   }
   __syncthreads();
   for (int u = threadIdx.x; u < nu; u += NT) {
@@ -252,7 +246,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
   __shared__ uint32_t s_hist[64];
   __shared__ uint32_t s_total;
   __shared__ uint32_t s_dense;
-  __shared__ uint32_t s_split[2];
+  __shared__ uint32_t s_split;
   __shared__ double s_wmax[G];
   __shared__ uint32_t s_red[G];
   __shared__ uint64_t s_mask[kUnits];
@@ -360,7 +354,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
       if (c) atomicAdd(&s_hist[64 - c], 1u);
     }
     const int nu2 = deal_units<NT>(nu, s_bucket, s_hist, s_order, &s_total, WAVE ? kWaveMin : 65, &s_dense,
-                                   WAVE ? nullptr : s_split);
+                                   WAVE ? nullptr : &s_split);
 
     int o0 = 0;
     if constexpr (WAVE) {
@@ -424,29 +418,17 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
       o0 = nd;
     }
 
-    // Slots: 4 per unit of the first n4 in the order, 2 per unit of the next
-    // n2, 1 per remaining unit; groups are aligned since s only decreases
-    // along the order.  Rounds are block-uniform so that every lane of a wave
-    // reaches the cross-lane sums.
-    const int n4 = WAVE ? 0 : int(s_split[0]), n2 = WAVE ? 0 : int(s_split[1]) - n4;
-    const int nslots = 4 * n4 + 2 * n2 + (nu2 - o0 - n4 - n2);
+    // Slots: 2 per unit of the first n2 in the order (the shared units), 1 per
+    // remaining unit; pairs start at even slots.  Rounds are block-uniform so
+    // that every lane of a wave reaches the cross-lane sums.
+    const int n2 = WAVE ? 0 : int(s_split);
+    const int nslots = 2 * n2 + (nu2 - o0 - n2);
     for (int sb = 0; sb < nslots; sb += NT) {
       const int slot = sb + tid;
       const bool live = slot < nslots;
-      int o, j = 0, gs = 1;
-      if (slot < 4 * n4) {
-        o = slot >> 2;
-        j = slot & 3;
-        gs = 4;
-      } else if (slot < 4 * n4 + 2 * n2) {
-        const int q = slot - 4 * n4;
-        o = n4 + (q >> 1);
-        j = q & 1;
-        gs = 2;
-      } else {
-        o = n4 + n2 + (slot - 4 * n4 - 2 * n2);
-      }
-      o = live ? o0 + o : o0;
+      const bool paired = slot < 2 * n2;
+      const int j = paired ? (slot & 1) : 0;
+      const int o = live ? o0 + (paired ? slot >> 1 : slot - n2) : o0;
       const int u = s_order[o], g = u % G;
       const uint32_t i = s_id[u / G];
       const double* Gm = A.geom + int64_t(kGeomStride) * i;
@@ -476,7 +458,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
       // (L,T) loads are all issued before its first hit is evaluated, so one
       // memory latency is paid per batch (no load is pending across
       // iterations, which would make the compiler wait for it early).
-      uint64_t m = live ? rank_subset(s_mask[u], gs, j) : 0ull;
+      uint64_t m = !live ? 0ull : paired ? rank_half(s_mask[u], j) : s_mask[u];
       while (m) {
         int bb[kBatch];
         uint4 lv[kBatch];
@@ -516,20 +498,13 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
             hit_grad_acc<K, FMT>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
         }
       }
-      // Partial sums of a group, added across its lanes (a no-op for lanes
-      // on their own; skipped by waves without groups).
-      if (__ballot(gs > 1)) {
+      // Partial sums of a pair, added across its two lanes (skipped by waves
+      // without pairs; lanes on their own keep theirs).
+      if (__ballot(paired)) {
 #pragma unroll
         for (int v = 0; v < AW; ++v) {
-          const float t = quad_swap<0xb1>(acc[v]);
-          acc[v] += gs > 1 ? t : 0.0f;
-        }
-        if (__ballot(gs > 2)) {
-#pragma unroll
-          for (int v = 0; v < AW; ++v) {
-            const float t = quad_swap<0x4e>(acc[v]);
-            acc[v] += gs > 2 ? t : 0.0f;
-          }
+          const float t = pair_swap(acc[v]);
+          acc[v] += paired ? t : 0.0f;
         }
       }
       if (!live || j != 0) continue;
