@@ -210,18 +210,31 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
       __syncthreads();
       if (!done && !finished && !stalled) {
         for (int c = 0; c < nb; ++c) {
+          // The candidate's whole staged row is read at once (one LDS round
+          // trip; every lane reads the same address), then the rectangle
+          // decides which lanes test it.
           const double* row = s_row + c * kRow;
           const int4 r = *reinterpret_cast<const int4*>(row + 16);
-          if (uint32_t(base - beg) + uint32_t(c) >= from && px >= r.x && px <= r.z && py >= r.y && py <= r.w) {
+          double W[9], og[3];
+#pragma unroll
+          for (int k = 0; k < 9; ++k) W[k] = row[k];
+#pragma unroll
+          for (int k = 0; k < 3; ++k) og[k] = row[9 + k];
+          double D2c = row[12], sig = row[13];
+          uint32_t id = reinterpret_cast<const uint32_t*>(row + 18)[0];
+          // materialise the row here, so that the compiler does not sink its
+          // reads into the branch (a second LDS round trip per candidate)
+#pragma unroll
+          for (int k = 0; k < 9; ++k) asm volatile("" : "+v"(W[k]));
+#pragma unroll
+          for (int k = 0; k < 3; ++k) asm volatile("" : "+v"(og[k]));
+          asm volatile("" : "+v"(D2c), "+v"(sig), "+v"(id));
+          const bool inside = (uint32_t(base - beg) + uint32_t(c) >= from) & (px >= r.x) & (px <= r.z) &
+                              (py >= r.y) & (py <= r.w);
+          if (inside) {
             ++n_tests;
-            double W[9], og[3];
-#pragma unroll
-            for (int k = 0; k < 9; ++k) W[k] = row[k];
-#pragma unroll
-            for (int k = 0; k < 3; ++k) og[k] = row[9 + k];
             double tau, D2, xg[3];
-            const uint32_t id = reinterpret_cast<const uint32_t*>(row + 18)[0];
-            if (ray_hit(W, og, row[12], d, &tau, &D2, xg) && key_less(last_tau, last_id, tau, id)) {
+            if (ray_hit(W, og, D2c, d, &tau, &D2, xg) && key_less(last_tau, last_id, tau, id)) {
               const uint32_t cpos = uint32_t(base - beg) + uint32_t(c);
               if (!key_less(tau, id, e_tau, e_id)) {
                 drop(tau, id, cpos);
@@ -237,7 +250,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
                   }
                 }
                 if (ins) {
-                  const double a = row[13] * exp(-0.5 * D2);
+                  const double a = sig * exp(-0.5 * D2);
                   // Position = entries with a smaller (depth, index) key.
                   // Unused slots hold depth +inf, so a strict depth count
                   // needs no occupancy test; equal depths (rare) also count
