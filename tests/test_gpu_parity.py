@@ -23,6 +23,10 @@ GROUPS = ["means", "log_scales", "quats", "logits", "sh"]
 def _scene(name):
     if name == "tiny":
         return make_scene("tiny")
+    if name == "small":  # the small workload at its full size, with its L1 upstream gradient
+        sc = make_scene("small")
+        sc.dl_dimage = l1_upstream(sc, oracle)
+        return sc
     if name == "small_reduced":
         sc = make_scene("small", n=30000, width=203, height=157)
         sc.dl_dimage = l1_upstream(sc, oracle)
@@ -67,7 +71,7 @@ def _case(name, mode="gather", tile=None):
     return _cache[("scene", name)], o, info, ren, grads, _cache[key]
 
 
-SCENES = ["tiny", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3", "random_sh1", "random_sh2",
+SCENES = ["tiny", "small", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3", "random_sh1", "random_sh2",
           "random_sh3_tile16"]
 
 
