@@ -797,7 +797,10 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 #ifndef GART_REDUCE_GAUSSIANS
 #define GART_REDUCE_GAUSSIANS 64
 #endif
-constexpr int kReduceLanes = 16;
+#ifndef GART_REDUCE_LANES
+#define GART_REDUCE_LANES 16
+#endif
+constexpr int kReduceLanes = GART_REDUCE_LANES;  // lanes per Gaussian in the row sum
 constexpr int kReduceBlock = GART_REDUCE_BLOCK;
 constexpr int kReduceGaussians = GART_REDUCE_GAUSSIANS;
 
@@ -805,24 +808,35 @@ template <int K, bool ROWS>
 __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs A) {
   constexpr int AS = acc_stride(K), NQ = AS / 4;
   constexpr int GROUPS = kReduceBlock / kReduceLanes;
-  static_assert(NQ <= kReduceLanes, "accumulator row wider than a lane group");
+  constexpr int NC = (NQ + kReduceLanes - 1) / kReduceLanes;  // float4 columns per lane
+  constexpr int kFlagStep = 16;                                // row flags read per step
+  static_assert(64 % kReduceLanes == 0 && kFlagStep % kReduceLanes == 0, "lane groups inside a wave");
   __shared__ __align__(16) float s_acc[kReduceGaussians][AS];
   const int64_t i0 = int64_t(blockIdx.x) * kReduceGaussians;
   const int grp = threadIdx.x / kReduceLanes, q = threadIdx.x % kReduceLanes;
-  const int shift = (threadIdx.x % 64) / kReduceLanes * kReduceLanes;
+  const int shift = (threadIdx.x % 64) / kReduceLanes * kReduceLanes;  // the group's first lane in its wave
 
   for (int gl = grp; gl < kReduceGaussians; gl += GROUPS) {
     const int64_t i = i0 + gl;
     const bool live = i < A.n;
     const uint32_t tc = live ? A.tile_count[i] : 0u;
-    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    float4 a[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) a[c] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if constexpr (ROWS) {
       const float4* rows = reinterpret_cast<const float4*>(A.rows);
       const int64_t r0 = live ? A.pair_offset[i] * A.rows_per_pair : 0, r1 = r0 + int64_t(tc) * A.rows_per_pair;
-      for (int64_t rb = r0; rb < r1; rb += kReduceLanes) {
-        const int64_t rq = rb + q;
-        const bool act = rq < r1 && A.row_flag[rq] != 0;
-        uint32_t m = uint32_t(__ballot(act) >> shift) & 0xffffu;
+      for (int64_t rb = r0; rb < r1; rb += kFlagStep) {
+        // lane q reads flags q, q + L, q + 2L, ... of the step; bit f of m is
+        // row rb + f
+        uint32_t m = 0;
+#pragma unroll
+        for (int t = 0; t < kFlagStep / kReduceLanes; ++t) {
+          const int64_t rq = rb + q + t * kReduceLanes;
+          const bool act = rq < r1 && A.row_flag[rq] != 0;
+          const uint32_t b = uint32_t(__ballot(act) >> shift) & ((1u << kReduceLanes) - 1u);
+          m |= b << (t * kReduceLanes);
+        }
         while (m) {
           int k[4];
 #pragma unroll
@@ -830,23 +844,37 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
             k[u] = m ? __ffs(m) - 1 : -1;
             m &= m ? m - 1 : 0u;
           }
-          float4 v[4];
+          float4 v[4][NC];
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            v[u] = (k[u] >= 0 && q < NQ) ? rows[(rb + k[u]) * NQ + q] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            a.x += v[u].x;
-            a.y += v[u].y;
-            a.z += v[u].z;
-            a.w += v[u].w;
-          }
+            for (int c = 0; c < NC; ++c) {
+              const int col = q + c * kReduceLanes;
+              v[u][c] = (k[u] >= 0 && col < NQ) ? rows[(rb + k[u]) * NQ + col] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+              a[c].x += v[u][c].x;
+              a[c].y += v[u][c].y;
+              a[c].z += v[u][c].z;
+              a[c].w += v[u][c].w;
+            }
         }
       }
-    } else if (live && tc && q < NQ) {
-      a = reinterpret_cast<const float4*>(A.acc)[i * NQ + q];
+    } else if (live && tc) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int col = q + c * kReduceLanes;
+        if (col < NQ) a[c] = reinterpret_cast<const float4*>(A.acc)[i * NQ + col];
+      }
     }
-    if (q < NQ) reinterpret_cast<float4*>(s_acc[gl])[q] = a;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int col = q + c * kReduceLanes;
+      if (col < NQ) reinterpret_cast<float4*>(s_acc[gl])[col] = a[c];
+    }
   }
   __syncthreads();
 
