@@ -816,16 +816,30 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
   const int grp = threadIdx.x / kReduceLanes, q = threadIdx.x % kReduceLanes;
   const int shift = (threadIdx.x % 64) / kReduceLanes * kReduceLanes;  // the group's first lane in its wave
 
-  for (int gl = grp; gl < kReduceGaussians; gl += GROUPS) {
+  // the row ranges of this group's Gaussians, loaded together up front
+  constexpr int kPer = (kReduceGaussians + GROUPS - 1) / GROUPS;
+  uint32_t tcs[kPer];
+  int64_t offs[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int64_t i = i0 + grp + int64_t(k) * GROUPS;
+    const bool live = grp + k * GROUPS < kReduceGaussians && i < A.n;
+    tcs[k] = live ? A.tile_count[i] : 0u;
+    offs[k] = (ROWS && live) ? A.pair_offset[i] : 0;
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int gl = grp + k * GROUPS;
+    if (gl >= kReduceGaussians) break;
     const int64_t i = i0 + gl;
     const bool live = i < A.n;
-    const uint32_t tc = live ? A.tile_count[i] : 0u;
+    const uint32_t tc = tcs[k];
     float4 a[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) a[c] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if constexpr (ROWS) {
       const float4* rows = reinterpret_cast<const float4*>(A.rows);
-      const int64_t r0 = live ? A.pair_offset[i] * A.rows_per_pair : 0, r1 = r0 + int64_t(tc) * A.rows_per_pair;
+      const int64_t r0 = offs[k] * A.rows_per_pair, r1 = r0 + int64_t(tc) * A.rows_per_pair;
       for (int64_t rb = r0; rb < r1; rb += kFlagStep) {
         // lane q reads flags q, q + L, q + 2L, ... of the step; bit f of m is
         // row rb + f
