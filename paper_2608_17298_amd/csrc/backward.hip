@@ -816,6 +816,19 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
   const int grp = threadIdx.x / kReduceLanes, q = threadIdx.x % kReduceLanes;
   const int shift = (threadIdx.x % 64) / kReduceLanes * kReduceLanes;  // the group's first lane in its wave
 
+  // The chain rule's own inputs (thread t < 64 serves Gaussian i0 + t), read
+  // now so that their latency overlaps the row sums.
+  float cq[4] = {1.0f, 0.0f, 0.0f, 0.0f}, cls[3] = {0.0f, 0.0f, 0.0f}, clg = 0.0f;
+  uint32_t ctc = 0;
+  if (int64_t(threadIdx.x) < min<int64_t>(kReduceGaussians, A.n - i0)) {
+    const int64_t ic = i0 + threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) cq[k] = A.quats[4 * ic + k];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) cls[k] = A.log_scales[3 * ic + k];
+    clg = A.logits[ic];
+    ctc = A.tile_count[ic];
+  }
   // the row ranges of this group's Gaussians, loaded together up front
   constexpr int kPer = (kReduceGaussians + GROUPS - 1) / GROUPS;
   uint32_t tcs[kPer];
@@ -903,13 +916,13 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
   float* gm = A.g_means + 3 * i;
   float* gs = A.g_log_scales + 3 * i;
   float* gq = A.g_quats + 4 * i;
-  if (A.tile_count[i] == 0) {  // culled: no ray can reach it (its sums are zero)
+  if (ctc == 0) {  // culled: no ray can reach it (its sums are zero)
     for (int k = 0; k < 3; ++k) gm[k] = gs[k] = 0.0f;
     for (int k = 0; k < 4; ++k) gq[k] = 0.0f;
     A.g_logits[i] = 0.0f;
     return;
   }
-  const double qw0 = A.quats[4 * i], qx0 = A.quats[4 * i + 1], qy0 = A.quats[4 * i + 2], qz0 = A.quats[4 * i + 3];
+  const double qw0 = cq[0], qx0 = cq[1], qy0 = cq[2], qz0 = cq[3];
   const double inv_qn = 1.0 / sqrt(qw0 * qw0 + qx0 * qx0 + qy0 * qy0 + qz0 * qz0);
   const double w = qw0 * inv_qn, x = qx0 * inv_qn, y = qy0 * inv_qn, z = qz0 * inv_qn;
   const double R[3][3] = {{1.0 - 2.0 * (y * y + z * z), 2.0 * (x * y - w * z), 2.0 * (x * z + w * y)},
@@ -918,7 +931,7 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
   double s[3], is[3];
 #pragma unroll
   for (int k = 0; k < 3; ++k) {
-    s[k] = exp(double(A.log_scales[3 * i + k]));
+    s[k] = exp(double(cls[k]));
     is[k] = 1.0 / s[k];
   }
   const double go[3] = {acc[0], acc[1], acc[2]};
@@ -950,7 +963,7 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
   const double qv[4] = {w, x, y, z};
 #pragma unroll
   for (int k = 0; k < 4; ++k) gq[k] = float((dq[k] - qv[k] * proj) * inv_qn);
-  const double sig = 1.0 / (1.0 + exp(-double(A.logits[i])));  // as in the bounds kernel
+  const double sig = 1.0 / (1.0 + exp(-double(clg)));  // as in the bounds kernel
   A.g_logits[i] = float(sig * (1.0 - sig) * double(acc[9]));
 }
 
