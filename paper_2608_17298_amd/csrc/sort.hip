@@ -114,10 +114,13 @@ hipError_t scan_impl(const T* in, T* out, int64_t n, T* total, char* tmp, hipStr
 
 // ---------------------------------------------------------------------------
 // Radix sort, 8-bit digits.  Pass = per-block digit histogram (digit-major
-// layout), exclusive scan of the histogram, stable scatter.  The scatter
-// ranks each round of 256 keys with wave64 ballots (peers holding the same
-// digit) plus per-wave counts in LDS, stages the block's keys in LDS in
-// digit order and writes them out as contiguous runs per digit.
+// layout), exclusive scan of the histogram, stable scatter.  In the scatter
+// each wave owns a contiguous quarter of the block's keys and ranks them on
+// its own, 64 at a time: wave64 ballots find the peers holding the same digit
+// and a per-wave running count per digit in LDS carries the rank across
+// rounds, so the rounds need no block barrier.  One block-wide scan then turns
+// the per-wave counts into offsets; the block's keys are staged in LDS in
+// digit order and written out as contiguous runs per digit.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t m,
                                                                   int shift, uint32_t* __restrict__ counts,
@@ -140,8 +143,7 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     uint32_t* __restrict__ vout, int64_t m, int shift, const uint32_t* __restrict__ offsets, int nblocks) {
   __shared__ uint32_t s_keys[kSortTile];
   __shared__ uint32_t s_vals[kSortTile];
-  __shared__ uint32_t s_run[256];
-  __shared__ uint32_t s_wave[kWaves][256];
+  __shared__ uint32_t s_wave[kWaves][256];  // per-wave digit counts, later per-wave digit bases
   __shared__ uint32_t s_start[256];
   __shared__ uint32_t s_gofs[256];
   __shared__ uint32_t s_wsum[kWaves];
@@ -151,21 +153,29 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
   const unsigned lane = __lane_id();
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-  s_run[tid] = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) s_wave[w][tid] = 0;
   s_gofs[tid] = offsets[int64_t(tid) * nblocks + blockIdx.x];
   __syncthreads();
 
-  const int64_t base = int64_t(blockIdx.x) * kSortTile;
+  // Keys [wbase, wbase + 64 * kSortItems) belong to this wave, so block order
+  // is wave, round, lane: the order of the input.
+  const int64_t wbase = int64_t(blockIdx.x) * kSortTile + int64_t(wave) * (64 * kSortItems);
   uint32_t myk[kSortItems], myv[kSortItems], myr[kSortItems];
 #pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
-    const int64_t j = base + int64_t(r) * kSortThreads + tid;
-    const bool valid = j < m;
-    const uint32_t k = valid ? kin[j] : 0u;
-    const uint32_t v = valid ? vin[j] : 0u;
-    const uint32_t d = (k >> shift) & 255u;
+    const int64_t j = wbase + int64_t(r) * 64 + lane;
+    myk[r] = j < m ? kin[j] : 0u;
+    myv[r] = j < m ? vin[j] : 0u;
+  }
+  // The running counts are read and updated by different lanes of one wave;
+  // LDS executes a wave's accesses in issue order, and volatile keeps the
+  // compiler from reordering or caching them.
+  volatile uint32_t* wcount = s_wave[wave];
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const bool valid = wbase + int64_t(r) * 64 + lane < m;
+    const uint32_t d = (myk[r] >> shift) & 255u;
     uint64_t peers = __ballot(valid);
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
@@ -174,31 +184,21 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
       peers &= bit ? bal : ~bal;
     }
     const uint32_t below = __popcll(peers & lt_mask);
-    if (valid && below == 0) s_wave[wave][d] = __popcll(peers);
-    __syncthreads();
-    uint32_t rank = 0;
-    if (valid) {
-      rank = s_run[d] + below;
-      for (int w = 0; w < wave; ++w) rank += s_wave[w][d];
-    }
-    __syncthreads();
-    uint32_t add = 0;
+    const uint32_t before = wcount[d];
+    myr[r] = before + below;
+    if (valid && below == 0) wcount[d] = before + uint32_t(__popcll(peers));
+  }
+  __syncthreads();
+
+  // Digit tid: block-exclusive start over digits, then each wave's base.
+  {
+    uint32_t c[kWaves], total = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      add += s_wave[w][tid];
-      s_wave[w][tid] = 0;
+      c[w] = s_wave[w][tid];
+      total += c[w];
     }
-    s_run[tid] += add;
-    __syncthreads();
-    myk[r] = k;
-    myv[r] = v;
-    myr[r] = rank;
-  }
-
-  // Block-local exclusive scan of the digit counts.
-  {
-    const uint32_t c = s_run[tid];
-    uint32_t inc = c;
+    uint32_t inc = total;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const uint32_t u = __shfl_up(inc, off);
@@ -208,22 +208,28 @@ __global__ __launch_bounds__(kSortThreads) void radix_scatter_kernel(
     __syncthreads();
     uint32_t before = 0;
     for (int w = 0; w < wave; ++w) before += s_wsum[w];
-    s_start[tid] = before + inc - c;
+    uint32_t run = before + inc - total;
+    s_start[tid] = run;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      s_wave[w][tid] = run;
+      run += c[w];
+    }
   }
   __syncthreads();
 
 #pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
-    const int64_t j = base + int64_t(r) * kSortThreads + tid;
-    if (j < m) {
+    if (wbase + int64_t(r) * 64 + lane < m) {
       const uint32_t d = (myk[r] >> shift) & 255u;
-      const uint32_t pos = s_start[d] + myr[r];
+      const uint32_t pos = s_wave[wave][d] + myr[r];
       s_keys[pos] = myk[r];
       s_vals[pos] = myv[r];
     }
   }
   __syncthreads();
 
+  const int64_t base = int64_t(blockIdx.x) * kSortTile;
   const int cnt = int(std::min<int64_t>(kSortTile, m - base));
   for (int q = tid; q < cnt; q += kSortThreads) {
     const uint32_t k = s_keys[q];
