@@ -327,17 +327,21 @@ __device__ __forceinline__ float depth_code_value(uint32_t c, int bits) {
 constexpr int kEmitGaussians = 256;
 
 __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
-  __shared__ int64_t s_base[kEmitGaussians + 1];
-  __shared__ int32_t s_rect[kEmitGaussians][4];
+  __shared__ uint32_t s_base[kEmitGaussians + 1];  // first pair slot, relative to the block's first
+  __shared__ int32_t s_tile[kEmitGaussians][3];     // first tile column, first tile row, tile columns
   __shared__ double s_q[kEmitGaussians][10];  // M (m00 m01 m02 m11 m12 m22), n (3), the Gaussian's bound
   const int64_t i0 = int64_t(blockIdx.x) * kEmitGaussians;
   const int nr = int(std::min<int64_t>(kEmitGaussians, A.n - i0));
-  for (int k = threadIdx.x; k <= nr; k += blockDim.x) s_base[k] = A.pair_offset[i0 + k];
+  const int ts = A.tile;
+  const int64_t first = A.pair_offset[i0];
+  for (int k = threadIdx.x; k <= nr; k += blockDim.x) s_base[k] = uint32_t(A.pair_offset[i0 + k] - first);
   for (int k = threadIdx.x; k < nr; k += blockDim.x) {
     const int64_t i = i0 + k;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) s_rect[k][c] = A.rect[4 * i + c];
     if (A.tile_count[i] == 0) continue;
+    const int tx0 = A.rect[4 * i] / ts;
+    s_tile[k][0] = tx0;
+    s_tile[k][1] = A.rect[4 * i + 1] / ts;
+    s_tile[k][2] = A.rect[4 * i + 2] / ts - tx0 + 1;
     const double* G = A.geom + int64_t(kGeomStride) * i;
     // P = W Rt maps (a, b, 1) to d_g = W d (Rt: camera -> world)
     double P[9];
@@ -361,20 +365,20 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
     s_q[k][9] = G[kGeoKey];
   }
   __syncthreads();
-  const int64_t first = s_base[0], last = s_base[nr];
-  const int ts = A.tile;
+  const uint32_t count = s_base[nr];
   const double ifx = 1.0 / A.cam.fx, ify = 1.0 / A.cam.fy;
-  for (int64_t j = first + threadIdx.x; j < last; j += blockDim.x) {
-    int lo = 0, hi = nr - 1;  // largest k with s_base[k] <= j
+  for (uint32_t jr = threadIdx.x; jr < count; jr += blockDim.x) {
+    int lo = 0, hi = nr - 1;  // largest k with s_base[k] <= jr
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      if (s_base[mid] <= j) lo = mid; else hi = mid - 1;
+      if (s_base[mid] <= jr) lo = mid; else hi = mid - 1;
     }
     const int k = lo;
-    const int64_t q = j - s_base[k];
-    const int tx0 = s_rect[k][0] / ts, ty0 = s_rect[k][1] / ts, tx1 = s_rect[k][2] / ts;
-    const int ntx = tx1 - tx0 + 1;
-    const int tx = tx0 + int(q % ntx), ty = ty0 + int(q / ntx);
+    const uint32_t q = jr - s_base[k];
+    const uint32_t ntx = uint32_t(s_tile[k][2]);
+    const uint32_t row = q / ntx;
+    const int tx = s_tile[k][0] + int(q - row * ntx), ty = s_tile[k][1] + int(row);
+    const int64_t j = first + jr;
     // the tile's pixel-centre rectangle in (a, b)
     const double a0 = (double(tx * ts) + 0.5 - A.cam.cx) * ifx;
     const double a1 = (double(min(A.cam.W - 1, tx * ts + ts - 1)) + 0.5 - A.cam.cx) * ifx;
