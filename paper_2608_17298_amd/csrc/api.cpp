@@ -307,7 +307,10 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   T.tile_count = f->tile_count;
   T.geom = f->prim_geom;
   T.pair_offset = f->pair_offset;
-  T.keys = f->pair_tile;
+  // Emission and the sort keep the combined keys in scratch; the last step
+  // splits them into pair_tile and pair_key.
+  uint32_t* sorted_keys = at<uint32_t>(f->scratch, L.pair_key_alt);
+  T.keys = sorted_keys;
   T.vals = f->pair_prim;
   T.pair_key = f->pair_key;
   T.pair_count = P;
@@ -322,12 +325,11 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   GART_HIP(scan_exclusive_i64(f->pair_offset, f->pair_offset, n, f->pair_offset + n, at<void>(f->scratch, L.scan_tmp), s));
   GART_HIP(launch_emit_pairs(T, s));
   GART_HIP(record(f->events[GART_EV_SORT_BEGIN], s));
-  GART_HIP(radix_sort_u32(f->pair_tile, f->pair_prim, at<uint32_t>(f->scratch, L.pair_key_alt),
-                          at<uint32_t>(f->scratch, L.pair_val_alt), P, tile_bits + T.key_bits,
-                          at<void>(f->scratch, L.radix_tmp), s));
+  GART_HIP(radix_sort_u32(sorted_keys, f->pair_prim, f->pair_tile, at<uint32_t>(f->scratch, L.pair_val_alt), P,
+                          tile_bits + T.key_bits, at<void>(f->scratch, L.radix_tmp), s));
   GART_HIP(record(f->events[GART_EV_SORT_END], s));
-  GART_HIP(launch_split_pair_keys(T, s));
-  GART_HIP(launch_tile_ranges(f->pair_tile, P, n_tiles, f->tile_range, s));
+  T.keys = f->pair_tile;
+  GART_HIP(launch_finish_pairs(T, sorted_keys, n_tiles, s));
   f->stage = 2;
   return GART_OK;
 }

@@ -403,22 +403,22 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
   }
 }
 
-__global__ void split_pair_keys_kernel(TileMapArgs A) {
+// One thread per sorted pair j, plus one for the end: splits the combined key
+// into the tile id and the decoded depth bound, and sets tile_range[t] = j for
+// every tile t after the previous pair's tile up to this pair's.
+__global__ void finish_pairs_kernel(TileMapArgs A, const uint32_t* __restrict__ sorted, int64_t n_tiles) {
   const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (j >= A.pair_count) return;
-  const uint32_t key = A.keys[j];
-  A.keys[j] = key >> A.key_bits;
-  A.pair_key[j] = depth_code_value(key & ((1u << A.key_bits) - 1u), A.key_bits);
-}
-
-// tile_range[t] = first sorted pair whose tile id is >= t.
-__global__ void tile_ranges_kernel(const uint32_t* __restrict__ keys, int64_t m, int64_t n_tiles,
-                                   int64_t* __restrict__ range) {
-  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t m = A.pair_count;
   if (j > m) return;
-  const int64_t prev = (j == 0) ? -1 : int64_t(keys[j - 1]);
-  const int64_t cur = (j == m) ? n_tiles : int64_t(keys[j]);
-  for (int64_t t = prev + 1; t <= cur && t <= n_tiles; ++t) range[t] = j;
+  const int64_t prev = (j == 0) ? -1 : int64_t(sorted[j - 1] >> A.key_bits);
+  int64_t cur = n_tiles;
+  if (j < m) {
+    const uint32_t key = sorted[j];
+    cur = int64_t(key >> A.key_bits);
+    A.keys[j] = uint32_t(cur);
+    A.pair_key[j] = depth_code_value(key & ((1u << A.key_bits) - 1u), A.key_bits);
+  }
+  for (int64_t t = prev + 1; t <= cur && t <= n_tiles; ++t) A.tile_range[t] = j;
 }
 
 }  // namespace
@@ -454,15 +454,8 @@ hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_split_pair_keys(const TileMapArgs& a, hipStream_t s) {
-  if (a.pair_count <= 0) return hipSuccess;
-  split_pair_keys_kernel<<<ceil_div(a.pair_count, 256), 256, 0, s>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_tile_ranges(const uint32_t* sorted_keys, int64_t pair_count, int64_t n_tiles, int64_t* tile_range,
-                              hipStream_t s) {
-  tile_ranges_kernel<<<ceil_div(pair_count + 1, 256), 256, 0, s>>>(sorted_keys, pair_count, n_tiles, tile_range);
+hipError_t launch_finish_pairs(const TileMapArgs& a, const uint32_t* sorted_keys, int64_t n_tiles, hipStream_t s) {
+  finish_pairs_kernel<<<ceil_div(a.pair_count + 1, 256), 256, 0, s>>>(a, sorted_keys, n_tiles);
   return hipGetLastError();
 }
 

@@ -81,10 +81,10 @@ struct TileMapArgs {
 };
 hipError_t launch_pair_counts(const TileMapArgs& a, hipStream_t s);
 hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s);
-// keys -> tile ids in place, and the decoded depth bound of each pair
-hipError_t launch_split_pair_keys(const TileMapArgs& a, hipStream_t s);
-hipError_t launch_tile_ranges(const uint32_t* sorted_keys, int64_t pair_count, int64_t n_tiles, int64_t* tile_range,
-                              hipStream_t s);
+// From the sorted combined keys (a buffer other than a.keys): a.keys[j] = tile
+// id, a.pair_key[j] = decoded depth bound, and a.tile_range[t] = first pair
+// whose tile id is >= t, for t in [0, n_tiles].
+hipError_t launch_finish_pairs(const TileMapArgs& a, const uint32_t* sorted_keys, int64_t n_tiles, hipStream_t s);
 
 // ---- forward.hip -------------------------------------------------------
 struct ForwardArgs {
