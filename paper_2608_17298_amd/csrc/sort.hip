@@ -1,4 +1,6 @@
-// Device-wide exclusive scans and a stable LSD radix sort for wave64.
+// Device-wide exclusive scans and a stable LSD radix sort for wave64.  A scan
+// is reduce-then-scan: block sums, then a down-sweep whose blocks add up the
+// sums before them (or, past 2048 blocks, a scan of the sums first).
 //
 // Used for the primitive offset table (prefix sum of footprints, Sec. 4.3),
 // the pair offsets, and the radix sort of (tile, primitive) pairs by tile id
@@ -70,10 +72,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const T* __re
   if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
+// Block offsets come either scanned (block_offset[b]) or as raw block sums,
+// which each block adds up for the blocks before it.
 template <typename T>
 __global__ __launch_bounds__(kScanThreads) void scan_down_kernel(const T* in, T* out, int64_t n,
                                                                  const T* __restrict__ block_offset,
-                                                                 T* __restrict__ total_out) {
+                                                                 T* __restrict__ total_out,
+                                                                 const T* __restrict__ block_sums) {
   const int64_t base = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
   T v[kScanItems];
   T s = 0;
@@ -82,9 +87,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_down_kernel(const T* in, T*
     v[k] = (base + k < n) ? in[base + k] : T(0);
     s += v[k];
   }
+  T off = block_offset ? block_offset[blockIdx.x] : T(0);
+  if (block_sums) {
+    T part = 0;
+    for (int k = threadIdx.x; k < int(blockIdx.x); k += kScanThreads) part += block_sums[k];
+    block_exclusive(part, &off);
+  }
   T total;
   T run = block_exclusive(s, &total);
-  const T off = block_offset ? block_offset[blockIdx.x] : T(0);
   run += off;
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
@@ -98,7 +108,7 @@ template <typename T>
 hipError_t scan_impl(const T* in, T* out, int64_t n, T* total, char* tmp, hipStream_t s) {
   const int64_t nb = std::max<int64_t>(1, ceil_div(n, kScanTile));
   if (nb == 1) {
-    scan_down_kernel<T><<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total);
+    scan_down_kernel<T><<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total, nullptr);
     return hipGetLastError();
   }
   T* sums = reinterpret_cast<T*>(tmp);
@@ -106,9 +116,13 @@ hipError_t scan_impl(const T* in, T* out, int64_t n, T* total, char* tmp, hipStr
   scan_reduce_kernel<T><<<nb, kScanThreads, 0, s>>>(in, n, sums);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (nb <= kScanTile) {  // few enough block sums for each block to add up its predecessors
+    scan_down_kernel<T><<<nb, kScanThreads, 0, s>>>(in, out, n, nullptr, total, sums);
+    return hipGetLastError();
+  }
   e = scan_impl<T>(sums, sums, nb, nullptr, rest, s);
   if (e != hipSuccess) return e;
-  scan_down_kernel<T><<<nb, kScanThreads, 0, s>>>(in, out, n, sums, total);
+  scan_down_kernel<T><<<nb, kScanThreads, 0, s>>>(in, out, n, sums, total, nullptr);
   return hipGetLastError();
 }
 
