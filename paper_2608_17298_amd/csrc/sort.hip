@@ -143,10 +143,16 @@ __global__ __launch_bounds__(kSortThreads) void radix_hist_kernel(const uint32_t
   h[threadIdx.x] = 0;
   __syncthreads();
   const int64_t base = int64_t(blockIdx.x) * kSortTile;
-#pragma unroll 4
+  uint32_t kv[kSortItems];
+#pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
     const int64_t j = base + int64_t(r) * kSortThreads + threadIdx.x;
-    if (j < m) atomicAdd(&h[(keys[j] >> shift) & 255u], 1u);
+    kv[r] = j < m ? keys[j] : 0u;
+  }
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const int64_t j = base + int64_t(r) * kSortThreads + threadIdx.x;
+    if (j < m) atomicAdd(&h[(kv[r] >> shift) & 255u], 1u);
   }
   __syncthreads();
   counts[int64_t(threadIdx.x) * nblocks + blockIdx.x] = h[threadIdx.x];
