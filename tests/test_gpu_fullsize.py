@@ -83,3 +83,40 @@ def test_fullsize_sampled(name, max_area):
     for k in GROUPS:
         e = rel_l2(gpu["grads"][k][sel], ref[k][sel])
         assert e <= GRAD_TOL, (k, e)
+
+
+def test_tile_map_past_two_level_scan():
+    """4.5 M Gaussians: more than 2048 scan blocks of 2048 items, so the
+    offset scans (primitive offsets, Eq. 15, and pair offsets) take their
+    two-level path. Checked against the oracle at every Gaussian (rectangle,
+    area and tile-count running sums) and on a sample of tiles' Gaussian
+    sets; tile ranges must bracket the sorted tile ids exactly."""
+    import torch
+    from paper_2608_17298_amd import gart
+    rng = np.random.default_rng(17298)
+    sc = make_scene("4m", n=4_500_000)
+    print(f"[4m, N={sc.n}] {sc.camera.width}x{sc.camera.height}", flush=True)
+    cam = gart.make_camera(sc.camera)
+    st = gart.make_settings(sc.tile, "gather")
+    g = gart.Gaussians.from_scene(sc)
+    frame = gart.prepare(g, cam, st)
+    torch.cuda.synchronize()
+    n, P = sc.n, frame.pair_count
+    o = oracle.OracleScene(sc)
+    info = o.prim_info()
+    W, H, ts = o.W, o.H, sc.tile
+    assert np.array_equal(frame.rect.cpu().numpy()[:n], info.rect)
+    lt = frame.lt_offset.cpu().numpy()[:n + 1]
+    assert lt[0] == 0 and np.array_equal(np.diff(lt), info.area)
+    tc = frame.tile_count.cpu().numpy()[:n].view(np.uint32).astype(np.int64)
+    po = frame.pair_offset.cpu().numpy()[:n + 1]
+    assert po[0] == 0 and po[n] == P and np.array_equal(np.diff(po), tc)
+    pair_tile = frame.pair_tile.cpu().numpy()[:P].view(np.uint32).astype(np.int64)
+    pair_prim = frame.pair_prim.cpu().numpy()[:P].view(np.uint32).astype(np.int64)
+    tr = frame.tile_range.cpu().numpy()
+    n_tiles = len(tr) - 1
+    assert np.all(np.diff(pair_tile) >= 0)
+    assert np.array_equal(tr, np.searchsorted(pair_tile, np.arange(n_tiles + 1), side="left"))
+    for t in rng.choice(n_tiles, 150, replace=False):
+        got = np.sort(pair_prim[tr[t]:tr[t + 1]])
+        assert np.array_equal(got, _brute_tile(info.rect, info.state, t, W, H, ts)), t
