@@ -321,8 +321,8 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   int tile_bits = 1;
   while ((int64_t(1) << tile_bits) < n_tiles) ++tile_bits;
   T.key_bits = std::min(24, 32 - tile_bits);
-  GART_HIP(launch_pair_counts(T, s));
-  GART_HIP(scan_exclusive_i64(f->pair_offset, f->pair_offset, n, f->pair_offset + n, at<void>(f->scratch, L.scan_tmp), s));
+  GART_HIP(scan_exclusive_u32_i64(f->tile_count, f->pair_offset, n, f->pair_offset + n,
+                                  at<void>(f->scratch, L.scan_tmp), s));
   GART_HIP(launch_emit_pairs(T, s));
   GART_HIP(record(f->events[GART_EV_SORT_BEGIN], s));
   GART_HIP(radix_sort_u32(sorted_keys, f->pair_prim, f->pair_tile, at<uint32_t>(f->scratch, L.pair_val_alt), P,

@@ -286,11 +286,6 @@ __global__ __launch_bounds__(256) void bounds_totals_kernel(const unsigned long 
   }
 }
 
-__global__ void pair_counts_kernel(TileMapArgs A) {
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < A.n) A.pair_offset[i] = A.tile_count[i];
-}
-
 // Depth bound <-> `bits`-bit code: the float at or below the bound, cut to
 // the 32 binary exponents of [2^-12, 2^20) (5 bits) and the leading
 // bits - 5 mantissa bits.  The code is monotone in the bound (the bits of a
@@ -439,12 +434,6 @@ hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s) {
 hipError_t launch_bounds_totals(const unsigned long long* block_partial, int64_t n_blocks, const int64_t* area_total,
                                 unsigned long long* totals, hipStream_t s) {
   bounds_totals_kernel<<<1, 256, 0, s>>>(block_partial, n_blocks, area_total, totals);
-  return hipGetLastError();
-}
-
-hipError_t launch_pair_counts(const TileMapArgs& a, hipStream_t s) {
-  if (a.n <= 0) return hipSuccess;
-  pair_counts_kernel<<<ceil_div(a.n, 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -18,6 +18,9 @@ namespace gart {
 size_t scan_tmp_bytes(int64_t n);
 hipError_t scan_exclusive_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp, hipStream_t s);
 hipError_t scan_exclusive_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total, void* tmp, hipStream_t s);
+// The same with 32-bit inputs and 64-bit sums (in and out are distinct).
+hipError_t scan_exclusive_u32_i64(const uint32_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp,
+                                  hipStream_t s);
 
 // Stable LSD radix sort of (key, value) pairs on key bits [0, bits), 8 bits
 // per pass.  The sorted pairs end in (keys, vals); (keys_alt, vals_alt) are
@@ -79,7 +82,6 @@ struct TileMapArgs {
   int64_t pair_count;
   int64_t* tile_range;      // [n_tiles+1]
 };
-hipError_t launch_pair_counts(const TileMapArgs& a, hipStream_t s);
 hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s);
 // From the sorted combined keys (a buffer other than a.keys): a.keys[j] = tile
 // id, a.pair_key[j] = decoded depth bound, and a.tile_range[t] = first pair

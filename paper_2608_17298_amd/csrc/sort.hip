@@ -59,14 +59,14 @@ __device__ __forceinline__ T block_exclusive(T v, T* block_total) {
   return before + inc - v;
 }
 
-template <typename T>
-__global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const T* __restrict__ in, int64_t n,
+template <typename Tin, typename T>
+__global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const Tin* __restrict__ in, int64_t n,
                                                                    T* __restrict__ sums) {
   const int64_t base = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
   T s = 0;
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k)
-    if (base + k < n) s += in[base + k];
+    if (base + k < n) s += T(in[base + k]);
   T total;
   block_exclusive(s, &total);
   if (threadIdx.x == 0) sums[blockIdx.x] = total;
@@ -74,8 +74,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce_kernel(const T* __re
 
 // Block offsets come either scanned (block_offset[b]) or as raw block sums,
 // which each block adds up for the blocks before it.
-template <typename T>
-__global__ __launch_bounds__(kScanThreads) void scan_down_kernel(const T* in, T* out, int64_t n,
+template <typename Tin, typename T>
+__global__ __launch_bounds__(kScanThreads) void scan_down_kernel(const Tin* in, T* out, int64_t n,
                                                                  const T* __restrict__ block_offset,
                                                                  T* __restrict__ total_out,
                                                                  const T* __restrict__ block_sums) {
@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_down_kernel(const T* in, T*
   T s = 0;
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
-    v[k] = (base + k < n) ? in[base + k] : T(0);
+    v[k] = (base + k < n) ? T(in[base + k]) : T(0);
     s += v[k];
   }
   T off = block_offset ? block_offset[blockIdx.x] : T(0);
@@ -104,25 +104,25 @@ __global__ __launch_bounds__(kScanThreads) void scan_down_kernel(const T* in, T*
   if (total_out && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *total_out = off + total;
 }
 
-template <typename T>
-hipError_t scan_impl(const T* in, T* out, int64_t n, T* total, char* tmp, hipStream_t s) {
+template <typename Tin, typename T>
+hipError_t scan_impl(const Tin* in, T* out, int64_t n, T* total, char* tmp, hipStream_t s) {
   const int64_t nb = std::max<int64_t>(1, ceil_div(n, kScanTile));
   if (nb == 1) {
-    scan_down_kernel<T><<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total, nullptr);
+    scan_down_kernel<Tin, T><<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total, nullptr);
     return hipGetLastError();
   }
   T* sums = reinterpret_cast<T*>(tmp);
   char* rest = tmp + ((nb * sizeof(T) + 255) & ~size_t(255));
-  scan_reduce_kernel<T><<<nb, kScanThreads, 0, s>>>(in, n, sums);
+  scan_reduce_kernel<Tin, T><<<nb, kScanThreads, 0, s>>>(in, n, sums);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (nb <= kScanTile) {  // few enough block sums for each block to add up its predecessors
-    scan_down_kernel<T><<<nb, kScanThreads, 0, s>>>(in, out, n, nullptr, total, sums);
+    scan_down_kernel<Tin, T><<<nb, kScanThreads, 0, s>>>(in, out, n, nullptr, total, sums);
     return hipGetLastError();
   }
-  e = scan_impl<T>(sums, sums, nb, nullptr, rest, s);
+  e = scan_impl<T, T>(sums, sums, nb, nullptr, rest, s);
   if (e != hipSuccess) return e;
-  scan_down_kernel<T><<<nb, kScanThreads, 0, s>>>(in, out, n, sums, total, nullptr);
+  scan_down_kernel<Tin, T><<<nb, kScanThreads, 0, s>>>(in, out, n, sums, total, nullptr);
   return hipGetLastError();
 }
 
@@ -301,12 +301,17 @@ size_t scan_tmp_bytes(int64_t n) {
 }
 
 hipError_t scan_exclusive_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp, hipStream_t s) {
-  return scan_impl<int64_t>(in, out, n, total, static_cast<char*>(tmp), s);
+  return scan_impl<int64_t, int64_t>(in, out, n, total, static_cast<char*>(tmp), s);
+}
+
+hipError_t scan_exclusive_u32_i64(const uint32_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp,
+                                  hipStream_t s) {
+  return scan_impl<uint32_t, int64_t>(in, out, n, total, static_cast<char*>(tmp), s);
 }
 
 hipError_t scan_exclusive_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total, void* tmp,
                               hipStream_t s) {
-  return scan_impl<uint32_t>(in, out, n, total, static_cast<char*>(tmp), s);
+  return scan_impl<uint32_t, uint32_t>(in, out, n, total, static_cast<char*>(tmp), s);
 }
 
 size_t radix_tmp_bytes(int64_t m) {
