@@ -15,6 +15,20 @@ def small_camera(w=32, h=32, distance=4.0):
     return pinhole_camera(w, h, 60.0, distance)
 
 
+def rotated_camera(w, h, axis=(1.0, 2.0, -0.5), angle_deg=35.0, distance=4.0):
+    """The 60 deg pinhole camera turned about the world origin by a rotation
+    about a non-axis-aligned axis (camera-to-world rotation Rot from scipy's
+    rotation-vector routine): centre Rot (0, 0, -distance), optical axis
+    Rot (0, 0, 1), so it still looks at the origin, with a roll.  World to
+    camera: R = Rot^T, t = (0, 0, distance)."""
+    from scipy.spatial.transform import Rotation
+    a = np.asarray(axis, np.float64)
+    rot = Rotation.from_rotvec(a / np.linalg.norm(a) * math.radians(angle_deg)).as_matrix()
+    cam = pinhole_camera(w, h, 60.0, distance)
+    cam.R = rot.T.astype(np.float32)
+    return cam
+
+
 def pixel_ray_point(cam: Camera, px, py, depth):
     """World point at camera depth ``depth`` on the ray through pixel centre (px, py).
 
@@ -32,9 +46,9 @@ def dc_for_colour(c):
 
 
 def random_tiny_scene(rng, n, w, h, deg, tile=8, spread=0.6, ls_mu=-2.3, ls_sd=0.25, logit_mu=0.0,
-                      logit_sd=1.0, high_sd=0.05):
+                      logit_sd=1.0, high_sd=0.05, cam=None):
     """A few Gaussians in front of the camera, sized to cover several pixels."""
-    cam = small_camera(w, h)
+    cam = small_camera(w, h) if cam is None else cam
     means = rng.uniform(-spread, spread, (n, 3))
     ls = rng.normal(ls_mu, ls_sd, (n, 3))
     q = rng.standard_normal((n, 4))
@@ -71,6 +85,7 @@ def run_gpu(scene, mode="gather", tile=None, dl=None, counters=True, keep_frame=
     frame = gart.prepare(g, cam, st, counters=counters)
     image = torch.empty((cam.height, cam.width, 3), dtype=torch.float32, device="cuda")
     gart.gart_forward(g, cam, st, frame, image)
+    assert gart.gart_frame_status(frame) == 0  # every ray traced to completion
     dlt = torch.from_numpy(np.ascontiguousarray(scene.dl_dimage if dl is None else dl, dtype=np.float32)).cuda()
     grads = gart.empty_grads(g)
     gart.gart_backward(g, cam, st, frame, dlt, grads)
@@ -100,3 +115,19 @@ def rel_l2(a, b):
     b = np.asarray(b, np.float64).ravel()
     nb = np.linalg.norm(b)
     return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+def per_gaussian_err(a, b, floor_frac=1e-3):
+    """Largest per-Gaussian relative error of one gradient group: rows are
+    Gaussians, |a_i - b_i| / max(|b_i|, floor) with the floor at floor_frac
+    times the RMS of the reference rows (a Gaussian whose gradient is a near
+    cancellation of its hits' terms is judged against the group's scale)."""
+    a = np.asarray(a, np.float64).reshape(len(a), -1)
+    b = np.asarray(b, np.float64).reshape(len(b), -1)
+    if b.size == 0:
+        return 0.0
+    nb = np.linalg.norm(b, axis=1)
+    rms = np.sqrt(np.mean(nb * nb))
+    if rms == 0.0:
+        return float(np.abs(a).max())
+    return float((np.linalg.norm(a - b, axis=1) / np.maximum(nb, floor_frac * rms)).max())
