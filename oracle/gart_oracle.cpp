@@ -690,6 +690,16 @@ void orc_backward(void* h, int64_t npix, const int64_t* pix, const double* dl_di
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i) {
     const Prim& P = S.prims[i];
+    if (P.state != kActive) {
+      // A culled Gaussian (R2; non-finite parameters) meets no ray, so every
+      // gradient of it is zero; the chain rule is not evaluated through
+      // parameters that may be non-finite.
+      for (int k = 0; k < 3; ++k) g_means[3 * i + k] = g_log_scales[3 * i + k] = 0.0;
+      for (int k = 0; k < 4; ++k) g_quats[4 * i + k] = 0.0;
+      g_logits[i] = 0.0;
+      for (int k = 0; k < K * 3; ++k) g_sh[i * K * 3 + k] = 0.0;
+      continue;
+    }
     const double* dW = &accW[9 * i];
     for (int k = 0; k < 3; ++k) g_means[3 * i + k] = accMu[3 * i + k];
     for (int k = 0; k < 3; ++k) {
