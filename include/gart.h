@@ -194,6 +194,10 @@ typedef struct {
                              a bound on every Gaussian's colour, divided by 2^32 */
   int32_t stage;          /* 0 none, 1 bounds, 2 tile map, 3 forward */
   int32_t lt_format;      /* gart_lt_format written by the last gart_forward */
+  int32_t width, height;  /* camera image size gart_bounds sized the frame for; later calls on
+                             the frame must pass a camera of this size (else INVALID_ARG) */
+  int32_t tile;           /* settings->tile gart_bounds used; later calls must use the same */
+  int32_t reserved;       /* set to 0 */
 } gart_frame;
 
 enum {
@@ -210,6 +214,14 @@ enum {
                                  of list positions that the tile needs) */
   GART_CNT_BWD_WAVE_UNITS = 10, /* units evaluated by a whole wave (GATHER_WAVE) */
   GART_NUM_COUNTERS = 16
+};
+
+/* Bits of the frame status word (see gart_frame_status). */
+enum {
+  GART_FRAME_STATUS_OK = 0,
+  GART_FRAME_FORWARD_INCOMPLETE = 1 /* the forward stopped tracing a tile at its safety limit on list
+                                       passes: image, intermediate buffer, hit_list and pixel_state of
+                                       that tile are incomplete (a library defect; never expected) */
 };
 
 enum {
@@ -367,6 +379,14 @@ gart_status gart_l1_loss_grad(const float* image, const float* target, int64_t n
  * (when n > 0), n < 0, step < 1 or hyper-parameters outside the ranges above. */
 gart_status gart_adam_step(float* param, const float* grad, float* m, float* v, int64_t n, const gart_adam* h,
                            int64_t step, void* stream);
+
+/* Frame status word: the GART_FRAME_* bits the kernels of the last
+ * gart_forward on this frame raised (0 = the forward traced every ray to
+ * completion).  The word lives in the frame's scratch; gart_forward clears
+ * it before tracing.  Copies it to *flags_host after synchronising stream.
+ * INVALID_ARG if frame or flags_host is NULL, or if gart_forward has not
+ * run on the frame. */
+gart_status gart_frame_status(const gart_frame* frame, uint32_t* flags_host, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* gart_status_string(gart_status status);

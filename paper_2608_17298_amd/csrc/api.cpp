@@ -39,7 +39,7 @@ gart_status fail(gart_status s, const char* fmt, ...) {
 size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, acc, rows, row_flag, total;
+  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, status, acc, rows, row_flag, total;
 };
 
 Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
@@ -57,6 +57,7 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
   L.scan_tmp = take(scan_tmp_bytes(nn + 1));
   L.totals = take(64);
   L.partials = take(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
+  L.status = take(4);
   const size_t AS = size_t(acc_stride(K));
   const bool rows = mode == GART_BACKWARD_GATHER || mode == GART_BACKWARD_GATHER_WAVE || mode == GART_BACKWARD_HYBRID;
   L.acc = take(rows ? 4 : size_t(nn) * AS * 4);
@@ -144,6 +145,97 @@ CamParams make_cam(const gart_camera* c) {
 
 int tiles_along(int pixels, int tile) { return (pixels + tile - 1) / tile; }
 
+// Later calls on a frame must describe the image and tiles gart_bounds sized
+// it for: the pixel state, the tile ranges and the hit lists are indexed with
+// them.
+gart_status check_frame_geometry(const gart_frame* f, const gart_camera* c, const gart_settings* s) {
+  GART_REQUIRE(c->width == f->width && c->height == f->height,
+               "camera is %dx%d but gart_bounds sized the frame for %dx%d", c->width, c->height, f->width,
+               f->height);
+  GART_REQUIRE(s->tile == f->tile, "settings tile %d differs from the %d gart_bounds used", s->tile, f->tile);
+  GART_REQUIRE(f->tiles_x == tiles_along(c->width, s->tile) && f->tiles_y == tiles_along(c->height, s->tile),
+               "frame tile grid %dx%d does not match the camera", f->tiles_x, f->tiles_y);
+  return GART_OK;
+}
+
+// Scratch regions of the bounds step, wherever they live (the frame's
+// scratch, or the library's static array).
+struct BoundsScratch {
+  void* scan_tmp;                 // area prefix-sum temporaries
+  unsigned long long* totals;     // 3 words: (L,T) entries, pairs, colour bound bits
+  unsigned long long* partials;   // 2 words per block of kBoundsBlock Gaussians
+};
+
+gart_status check_bounds_args(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                              const gart_frame* f) {
+  gart_status st;
+  if ((st = check_gaussians(g)) != GART_OK) return st;
+  if ((st = check_camera(camera)) != GART_OK) return st;
+  if ((st = check_settings(settings)) != GART_OK) return st;
+  GART_REQUIRE(f != nullptr, "frame is NULL");
+  GART_REQUIRE(f->lt_offset != nullptr, "frame lt_offset is NULL");
+  if (g->n > 0) GART_REQUIRE(f->rect && f->prim_geom && f->tile_count, "frame per-Gaussian buffer is NULL");
+  GART_REQUIRE(f->rect == nullptr || aligned16(f->rect), "rect must be 16-byte aligned");
+  return GART_OK;
+}
+
+// Per-Gaussian bounds, the area prefix sum and the totals, then the one host
+// synchronisation (arguments already checked).
+gart_status run_bounds(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                       gart_frame* f, int64_t* lt_entries_host, int64_t* pair_count_host, hipStream_t s,
+                       const BoundsScratch& S) {
+  const int64_t n = g->n;
+  const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
+  f->stage = 0;
+  BoundsArgs A{};
+  A.means = g->means;
+  A.log_scales = g->log_scales;
+  A.quats = g->quats;
+  A.logits = g->opacity_logits;
+  A.sh = g->sh;
+  A.K = K;
+  A.n = n;
+  A.cam = make_cam(camera);
+  A.alpha_min = settings->alpha_min;
+  A.tile = settings->tile;
+  A.rect = f->rect;
+  A.area = f->lt_offset;
+  A.geom = f->prim_geom;
+  A.tile_count = f->tile_count;
+  A.block_partial = S.partials;
+  GART_HIP(launch_bounds(A, s));
+  GART_HIP(scan_exclusive_i64(f->lt_offset, f->lt_offset, n, f->lt_offset + n, S.scan_tmp, s));
+  GART_HIP(launch_bounds_totals(A.block_partial, (n + kBoundsBlock - 1) / kBoundsBlock, f->lt_offset + n, S.totals,
+                                s));
+  unsigned long long tot[3] = {0, 0, 0};  // (L,T) entries, pairs, colour bound bits
+  GART_HIP(hipMemcpyAsync(tot, S.totals, sizeof tot, hipMemcpyDeviceToHost, s));
+  GART_HIP(hipStreamSynchronize(s));
+  const int64_t host[2] = {int64_t(tot[0]), int64_t(tot[1])};
+  float cb;
+  const uint32_t cb_bits = uint32_t(tot[2]);
+  std::memcpy(&cb, &cb_bits, sizeof cb);
+  f->color_step = double(cb > 0.0f ? cb : 1.0f) / 4294967296.0;
+
+  f->n = n;
+  f->sh_degree = g->sh_degree;
+  f->tiles_x = tiles_along(camera->width, settings->tile);
+  f->tiles_y = tiles_along(camera->height, settings->tile);
+  f->width = camera->width;
+  f->height = camera->height;
+  f->tile = settings->tile;
+  f->reserved = 0;
+  f->lt_entries = host[0];
+  f->pair_count = host[1];
+  if (lt_entries_host) *lt_entries_host = host[0];
+  if (pair_count_host) *pair_count_host = host[1];
+  if (host[0] > f->lt_capacity || host[1] > f->pair_capacity)
+    return fail(GART_ERR_CAPACITY, "need lt %lld (have %lld), pairs %lld (have %lld)", (long long)host[0],
+                (long long)f->lt_capacity, (long long)host[1], (long long)f->pair_capacity);
+  if (host[1] >= (int64_t(1) << 32)) return fail(GART_ERR_UNSUPPORTED, "more than 2^32 tile pairs");
+  f->stage = 1;
+  return GART_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -196,6 +288,22 @@ const char* gart_status_string(gart_status s) {
 
 const char* gart_last_error(void) { return g_err; }
 
+gart_status gart_frame_status(const gart_frame* f, uint32_t* flags_host, void* stream) {
+  g_err[0] = 0;
+  GART_REQUIRE(f != nullptr && flags_host != nullptr, "frame/flags_host is NULL");
+  GART_REQUIRE(f->stage >= 3, "gart_forward has not run on this frame");
+  const int K = (f->sh_degree + 1) * (f->sh_degree + 1);
+  // the status word's offset does not depend on the backward mode
+  const Layout L = make_layout(f->n, K, f->pair_capacity, GART_BACKWARD_GATHER, f->tile);
+  GART_REQUIRE(f->scratch != nullptr && f->scratch_bytes >= L.status + 4, "frame scratch is too small");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint32_t v = 0;
+  GART_HIP(hipMemcpyAsync(&v, at<uint32_t>(f->scratch, L.status), sizeof v, hipMemcpyDeviceToHost, s));
+  GART_HIP(hipStreamSynchronize(s));
+  *flags_host = v;
+  return GART_OK;
+}
+
 int32_t gart_lt_entry_bytes(const gart_settings* settings) {
   g_err[0] = 0;
   if (check_settings(settings) != GART_OK) return 0;
@@ -217,63 +325,17 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
                         gart_frame* f, int64_t* lt_entries_host, int64_t* pair_count_host, void* stream) {
   g_err[0] = 0;
   gart_status st;
-  if ((st = check_gaussians(g)) != GART_OK) return st;
-  if ((st = check_camera(camera)) != GART_OK) return st;
-  if ((st = check_settings(settings)) != GART_OK) return st;
-  GART_REQUIRE(f != nullptr, "frame is NULL");
+  if ((st = check_bounds_args(g, camera, settings, f)) != GART_OK) return st;
   const int64_t n = g->n;
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
-  GART_REQUIRE(f->lt_offset != nullptr && f->scratch != nullptr, "frame lt_offset/scratch is NULL");
-  if (n > 0) GART_REQUIRE(f->rect && f->prim_geom && f->tile_count, "frame per-Gaussian buffer is NULL");
-  GART_REQUIRE(f->rect == nullptr || aligned16(f->rect), "rect must be 16-byte aligned");
+  GART_REQUIRE(f->scratch != nullptr, "frame scratch is NULL");
   const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-
-  f->stage = 0;
-  unsigned long long* totals = at<unsigned long long>(f->scratch, L.totals);
-  BoundsArgs A{};
-  A.means = g->means;
-  A.log_scales = g->log_scales;
-  A.quats = g->quats;
-  A.logits = g->opacity_logits;
-  A.sh = g->sh;
-  A.K = K;
-  A.n = n;
-  A.cam = make_cam(camera);
-  A.alpha_min = settings->alpha_min;
-  A.tile = settings->tile;
-  A.rect = f->rect;
-  A.area = f->lt_offset;
-  A.geom = f->prim_geom;
-  A.tile_count = f->tile_count;
-  A.block_partial = at<unsigned long long>(f->scratch, L.partials);
-  GART_HIP(launch_bounds(A, s));
-  GART_HIP(scan_exclusive_i64(f->lt_offset, f->lt_offset, n, f->lt_offset + n, at<void>(f->scratch, L.scan_tmp), s));
-  GART_HIP(launch_bounds_totals(A.block_partial, (n + kBoundsBlock - 1) / kBoundsBlock, f->lt_offset + n, totals, s));
-  unsigned long long tot[3] = {0, 0, 0};  // (L,T) entries, pairs, colour bound bits
-  GART_HIP(hipMemcpyAsync(tot, totals, sizeof tot, hipMemcpyDeviceToHost, s));
-  GART_HIP(hipStreamSynchronize(s));
-  const int64_t host[2] = {int64_t(tot[0]), int64_t(tot[1])};
-  float cb;
-  const uint32_t cb_bits = uint32_t(tot[2]);
-  std::memcpy(&cb, &cb_bits, sizeof cb);
-  f->color_step = double(cb > 0.0f ? cb : 1.0f) / 4294967296.0;
-
-  f->n = n;
-  f->sh_degree = g->sh_degree;
-  f->tiles_x = tiles_along(camera->width, settings->tile);
-  f->tiles_y = tiles_along(camera->height, settings->tile);
-  f->lt_entries = host[0];
-  f->pair_count = host[1];
-  if (lt_entries_host) *lt_entries_host = host[0];
-  if (pair_count_host) *pair_count_host = host[1];
-  if (host[0] > f->lt_capacity || host[1] > f->pair_capacity)
-    return fail(GART_ERR_CAPACITY, "need lt %lld (have %lld), pairs %lld (have %lld)", (long long)host[0],
-                (long long)f->lt_capacity, (long long)host[1], (long long)f->pair_capacity);
-  if (host[1] >= (int64_t(1) << 32)) return fail(GART_ERR_UNSUPPORTED, "more than 2^32 tile pairs");
-  f->stage = 1;
-  return GART_OK;
+  BoundsScratch S;
+  S.scan_tmp = at<void>(f->scratch, L.scan_tmp);
+  S.totals = at<unsigned long long>(f->scratch, L.totals);
+  S.partials = at<unsigned long long>(f->scratch, L.partials);
+  return run_bounds(g, camera, settings, f, lt_entries_host, pair_count_host, static_cast<hipStream_t>(stream), S);
 }
 
 gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* settings, gart_frame* f,
@@ -284,9 +346,7 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   if ((st = check_settings(settings)) != GART_OK) return st;
   GART_REQUIRE(f != nullptr, "frame is NULL");
   GART_REQUIRE(f->stage >= 1, "gart_bounds must succeed on this frame first");
-  GART_REQUIRE(f->tiles_x == tiles_along(camera->width, settings->tile) &&
-                   f->tiles_y == tiles_along(camera->height, settings->tile),
-               "camera/tile differ from gart_bounds");
+  if ((st = check_frame_geometry(f, camera, settings)) != GART_OK) return st;
   const int64_t n = f->n, P = f->pair_count;
   const int64_t n_tiles = int64_t(f->tiles_x) * f->tiles_y;
   GART_REQUIRE(f->pair_offset && f->tile_range, "frame pair_offset/tile_range is NULL");
@@ -343,11 +403,16 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   if ((st = check_settings(settings)) != GART_OK) return st;
   GART_REQUIRE(f != nullptr, "frame is NULL");
   GART_REQUIRE(f->stage >= 2, "gart_build_tile_map must succeed on this frame first");
+  if ((st = check_frame_geometry(f, camera, settings)) != GART_OK) return st;
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(image != nullptr && f->pixel_state != nullptr, "image/pixel_state is NULL");
   GART_REQUIRE(f->lt_entries <= f->lt_capacity, "lt capacity");
   GART_REQUIRE(f->lt_entries == 0 || (f->lt != nullptr && aligned16(f->lt)), "lt must be non-NULL, 16-byte aligned");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
+  const int Kf = (f->sh_degree + 1) * (f->sh_degree + 1);
+  const Layout Lf = make_layout(f->n, Kf, f->pair_capacity, settings->backward_mode, settings->tile);
+  GART_REQUIRE(f->scratch != nullptr && f->scratch_bytes >= Lf.total, "scratch_bytes %zu < required %zu",
+               f->scratch_bytes, Lf.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
   ForwardArgs A{};
   A.cam = make_cam(camera);
@@ -372,6 +437,8 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.counters = f->counters;
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
+  A.status = at<uint32_t>(f->scratch, Lf.status);
+  GART_HIP(fill_u32(A.status, 0u, 1, s));
   GART_HIP(launch_forward(A, s));
   f->lt_format = A.lt_format;
   f->stage = 3;
@@ -388,6 +455,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   if ((st = check_settings(settings)) != GART_OK) return st;
   GART_REQUIRE(f != nullptr, "frame is NULL");
   GART_REQUIRE(f->stage >= 3, "gart_forward must succeed on this frame first");
+  if ((st = check_frame_geometry(f, camera, settings)) != GART_OK) return st;
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");

@@ -34,9 +34,9 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Adds the gradient contribution of one composited hit to acc (accumulator
 // layout), with explicit fused multiply-adds.
 template <int K, int FMT>
-__device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], double sigma, const float sh[3 * K],
-                                             const float Y[K], const uint32_t Cq[3], const float g[3], uint4 lt,
-                                             float step, float acc[acc_width(K)]) {
+__device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], double sigma, float one_minus_sigma,
+                                             const float sh[3 * K], const float Y[K], const uint32_t Cq[3],
+                                             const float g[3], uint4 lt, float step, float acc[acc_width(K)]) {
   // exp(-D2 / 2) as 2^(-D2 log2(e) / 2) on the hardware exp2 (about 1 ulp)
   const float rho = __builtin_amdgcn_exp2f(float(-0.72134752044448170368 * D2));
   const float a = float(sigma) * rho;
@@ -52,7 +52,7 @@ __device__ __forceinline__ void hit_grad_acc(double D2, const double xg[3], doub
   }
   const float T = lt_T<FMT>(lt);
   const float ta = T * a;
-  const float inv = __builtin_amdgcn_rcpf(1.0f - a);  // about 1 ulp
+  const float inv = inv_one_minus_alpha(one_minus_alpha(float(sigma), one_minus_sigma, float(0.5 * D2), rho));
   float dlda = 0.0f;
   float dc[3];
 #pragma unroll
@@ -378,6 +378,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
 #pragma unroll
           for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
           const double sigma = Gm[kGeoSigma];
+          const float oms = float(Gm[kGeoOneMinusSigma]);
           float sh[3 * K];
           const float* shp = A.sh + int64_t(i) * (3 * K);
 #pragma unroll
@@ -399,7 +400,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
           const float4 g4 = *reinterpret_cast<const float4*>(&s_cg[tid][4]);
           const uint32_t Cq[3] = {c4.x, c4.y, c4.z};
           const float gr[3] = {__uint_as_float(c4.w), g4.x, g4.y};
-          hit_grad_acc<K, FMT>(D2, xg, sigma, sh, Y, Cq, gr, lt, A.color_step, v);  // v[0 .. AW)
+          hit_grad_acc<K, FMT>(D2, xg, sigma, oms, sh, Y, Cq, gr, lt, A.color_step, v);  // v[0 .. AW)
           ++n_hits;
         }
         // lane e < 32: sum of value e; lane e >= 32: sum of value e
@@ -438,6 +439,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
 #pragma unroll
       for (int k = 0; k < 3; ++k) og[k] = Gm[kGeoOg + k];
       const double sigma = Gm[kGeoSigma];
+      const float oms = float(Gm[kGeoOneMinusSigma]);
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
       float sh[3 * K];
       const float* shp = A.sh + int64_t(i) * (3 * K);
@@ -495,7 +497,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
           if constexpr (HYBRID)
             hit_sh_acc<K>(D2, sigma, sh, Y, gr, lt_T<FMT>(lv[t]), acc);
           else
-            hit_grad_acc<K, FMT>(D2, xg, sigma, sh, Y, Cq, gr, lv[t], A.color_step, acc);
+            hit_grad_acc<K, FMT>(D2, xg, sigma, oms, sh, Y, Cq, gr, lv[t], A.color_step, acc);
         }
       }
       // Partial sums of a pair, added across its two lanes (skipped by waves
@@ -607,6 +609,7 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
 #pragma unroll
       for (int e = 0; e < 3; ++e) og[e] = Gm[kGeoOg + e];
       const double sigma = Gm[kGeoSigma];
+      const float oms = float(Gm[kGeoOneMinusSigma]);
       const int4 r = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(i));
       const float T = lt_T<FMT>(lt_load<FMT>(A.lt, A.lt_offset[i] + lt_local_index(r.x, r.y, r.z, r.w, TILE, px, py)));
       double D2, xg[3];
@@ -623,7 +626,7 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
         c[ch] = cv > 0.0f ? cv : 0.0f;
       }
       if (pos >= w0 && pos < w0 + kWin) {
-        const float inv = __builtin_amdgcn_rcpf(1.0f - a);
+        const float inv = inv_one_minus_alpha(one_minus_alpha(float(sigma), oms, float(0.5 * D2), rho));
         float dlda = 0.0f;
 #pragma unroll
         for (int ch = 0; ch < 3; ++ch) dlda = fmaf(g[ch], fmaf(T, c[ch], -float(S[ch]) * inv), dlda);
@@ -734,6 +737,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
       ri[2] = r.z;
       ri[3] = r.w;
       reinterpret_cast<uint32_t*>(row + 18)[0] = id;
+      row[19] = G[kGeoOneMinusSigma];
     }
     __syncthreads();
     if (!done) {
@@ -765,7 +769,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
         float h[AW];
 #pragma unroll
         for (int v = 0; v < AW; ++v) h[v] = 0.0f;
-        hit_grad_acc<K, FMT>(D2, xg, row[13], sh, Y, Cq, g, lt, A.color_step, h);
+        hit_grad_acc<K, FMT>(D2, xg, row[13], float(row[19]), sh, Y, Cq, g, lt, A.color_step, h);
         float* dst = A.acc + int64_t(id) * AS;
 #pragma unroll
         for (int v = 0; v < AW; ++v) unsafeAtomicAdd(dst + v, h[v]);

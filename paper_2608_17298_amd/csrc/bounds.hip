@@ -150,6 +150,7 @@ __global__ __launch_bounds__(kBoundsBlock) void bounds_kernel(BoundsArgs A) {
         }
         G[kGeoD2c] = D2c;
         G[kGeoSigma] = sigma;
+        G[kGeoOneMinusSigma] = 1.0 / (1.0 + exp(double(lg)));  // 1 - sigma without cancellation
         // Lower bound on the depth tau of any hit.  The max-response point
         // x = o + tau d lies in the clamped ellipsoid, hence within r =
         // alpha_c max(s) of mu, so tau >= |mu - o| - r.  Tighter: x is the

@@ -18,8 +18,9 @@ namespace gart {
 constexpr int kGeomStride = 16;  // doubles per Gaussian in prim_geom
 // prim_geom layout (double): [0..8] W = S^-1 R^T row-major, [9..11] o_g =
 // W (o - mu), [12] squared clamp radius D2c, [13] opacity sigma, [14] depth
-// lower bound (the float sort key, widened), [15] unused.
-constexpr int kGeoW = 0, kGeoOg = 9, kGeoD2c = 12, kGeoSigma = 13, kGeoKey = 14;
+// lower bound (the float sort key, widened), [15] 1 - sigma = sigmoid(-logit)
+// (so that 1 - alpha keeps its precision for nearly opaque Gaussians).
+constexpr int kGeoW = 0, kGeoOg = 9, kGeoD2c = 12, kGeoSigma = 13, kGeoKey = 14, kGeoOneMinusSigma = 15;
 
 constexpr uint32_t kNoPrim = 0xffffffffu;
 
@@ -94,6 +95,29 @@ __device__ __forceinline__ void hit_point(const double W[9], const double og[3],
 #pragma unroll
   for (int k = 0; k < 3; ++k) xg[k] = fma(tau, dg[k], og[k]);
   *D2_out = fma(xg[0], xg[0], fma(xg[1], xg[1], xg[2] * xg[2]));
+}
+
+// 1 - alpha for alpha = sigma rho, rho = exp(-x), x = D2 / 2, formed as
+// (1 - sigma) + sigma (1 - rho) from the Gaussian's own 1 - sigma, so that
+// it keeps its relative precision when alpha is close to 1 (1 - rho comes
+// from its Taylor series below x = 1/4, error under 2e-9 relative; above,
+// 1 - rho > 0.22 and the plain difference is exact to rounding).  Only
+// feeds gradients.
+__device__ __forceinline__ float one_minus_alpha(float sigma, float one_minus_sigma, float x, float rho) {
+  float t = fmaf(-x, 1.0f / 7.0f, 1.0f);
+  t = fmaf(-x * (1.0f / 6.0f), t, 1.0f);
+  t = fmaf(-x * (1.0f / 5.0f), t, 1.0f);
+  t = fmaf(-x * (1.0f / 4.0f), t, 1.0f);
+  t = fmaf(-x * (1.0f / 3.0f), t, 1.0f);
+  t = fmaf(-x * 0.5f, t, 1.0f);
+  const float om_rho = x < 0.25f ? x * t : 1.0f - rho;
+  return fmaf(sigma, om_rho, one_minus_sigma);
+}
+
+// 1 / (1 - alpha) for the colour-behind term S / (1 - alpha) of dL/dalpha;
+// 0 for a fully opaque hit (alpha = 1), which nothing behind can reach.
+__device__ __forceinline__ float inv_one_minus_alpha(float oma) {
+  return oma > 0.0f ? __builtin_amdgcn_rcpf(oma) : 0.0f;
 }
 
 // (tau, id) lexicographic order used to composite hits.

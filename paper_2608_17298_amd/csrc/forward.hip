@@ -315,7 +315,11 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
     __syncthreads();
     const unsigned rs = s_restart;
     __syncthreads();
-    if (rs == UINT_MAX || passes >= kMaxPasses) break;
+    if (rs == UINT_MAX) break;
+    if (passes >= kMaxPasses) {  // never expected: reported, not hidden
+      if (tid == 0) atomicOr(A.status, unsigned(GART_FRAME_FORWARD_INCOMPLETE));
+      break;
+    }
     restart = rs;
     ++passes;
     if (need) {

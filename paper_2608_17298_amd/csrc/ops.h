@@ -106,6 +106,7 @@ struct ForwardArgs {
   float* image;
   gart_pixel_state* pixel_state;
   uint32_t* hit_list;       // [pairs * tile^2] list position of each pixel's k-th composited hit
+  uint32_t* status;         // frame status word (GART_FRAME_* bits), cleared before the launch
   uint64_t* counters;
   void* ev_begin;  // optional hipEvent_t recorded around the kernel
   void* ev_end;

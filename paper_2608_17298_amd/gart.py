@@ -76,7 +76,8 @@ class gart_frame(ctypes.Structure):
                 ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
                 ("color_step", ctypes.c_double), ("stage", ctypes.c_int32),
-                ("lt_format", ctypes.c_int32)]
+                ("lt_format", ctypes.c_int32), ("width", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("tile", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class GartError(RuntimeError):
@@ -114,6 +115,8 @@ def lib():
         L.gart_forward.argtypes = [_P, _P, _P, _P, _P, _P]
         L.gart_backward.restype = ctypes.c_int
         L.gart_backward.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.gart_frame_status.restype = ctypes.c_int
+        L.gart_frame_status.argtypes = [_P, _P, _P]
         L.gart_status_string.restype = ctypes.c_char_p
         L.gart_status_string.argtypes = [ctypes.c_int]
         L.gart_last_error.restype = ctypes.c_char_p
@@ -364,6 +367,18 @@ def gart_bounds(g: Gaussians, camera: gart_camera, settings: gart_settings, fram
         raise GartCapacityError("gart_bounds", lib().gart_last_error().decode(), lt.value, pc.value)
     _check(st, "gart_bounds")
     return lt.value, pc.value
+
+
+FRAME_FORWARD_INCOMPLETE = 1
+
+
+def gart_frame_status(frame: Frame, stream=None) -> int:
+    """The frame status word (GART_FRAME_* bits) left by the last gart_forward;
+    synchronises the stream."""
+    fs = frame.c_struct()
+    v = ctypes.c_uint32(0)
+    _check(lib().gart_frame_status(ctypes.byref(fs), ctypes.byref(v), _stream(stream)), "gart_frame_status")
+    return int(v.value)
 
 
 def gart_build_tile_map(camera: gart_camera, settings: gart_settings, frame: Frame, stream=None):

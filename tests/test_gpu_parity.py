@@ -9,13 +9,19 @@ import numpy as np
 import pytest
 
 import oracle
-from helpers import dc_for_colour, l1_upstream, random_tiny_scene, rel_l2, run_gpu, small_camera
+from helpers import (dc_for_colour, l1_upstream, per_gaussian_err, random_tiny_scene, rel_l2, rotated_camera,
+                     run_gpu, small_camera)
 from paper_2608_17298_amd.scenes import custom_scene, make_scene
 
 pytestmark = pytest.mark.gpu
 
 PIX_TOL = 1e-5
 GRAD_TOL = 1e-4
+# Per-Gaussian bar: each hit's terms carry about 1e-6 relative error (fp32
+# colour, SH and accumulation; fp64 geometry), so a Gaussian's gradient errs
+# by about 1e-6 times the cancellation factor sum|terms| / |sum|; 1e-3
+# allows a factor of 1000 against max(|g_i|, 1e-3 x the group's RMS).
+ELEM_TOL = 1e-3
 AMBIG = 1e-9
 GROUPS = ["means", "log_scales", "quats", "logits", "sh"]
 
@@ -52,6 +58,39 @@ def _scene(name):
         sc, _, _ = random_tiny_scene(np.random.default_rng(7), 500, 97, 70, 3, tile=16, spread=1.0, ls_mu=-2.4,
                                      ls_sd=0.5, logit_mu=0.5)
         return sc
+    if name == "rotated_sh3":  # camera turned about a non-axis-aligned axis (with roll), SH3, 8x8 tiles
+        sc, _, _ = random_tiny_scene(np.random.default_rng(9), 600, 91, 67, 3, spread=1.0, ls_mu=-2.5, ls_sd=0.5,
+                                     logit_mu=0.5, high_sd=0.15, cam=rotated_camera(91, 67))
+        return sc
+    if name == "opaque_sh3":  # nearly opaque Gaussians: logits ~ N(10, 2), 1 - alpha down to ~1e-8
+        sc, _, _ = random_tiny_scene(np.random.default_rng(13), 400, 79, 61, 3, spread=1.0, ls_mu=-2.4,
+                                     ls_sd=0.5, logit_mu=10.0, logit_sd=2.0, cam=rotated_camera(79, 61))
+        return sc
+    if name == "nonfinite_sh3":  # NaN / inf parameters and zero-norm quaternions among ordinary Gaussians
+        rng = np.random.default_rng(17)
+        sc, _, _ = random_tiny_scene(rng, 400, 73, 59, 3, spread=1.0, ls_mu=-2.5, ls_sd=0.5, logit_mu=0.5)
+        bad = rng.choice(sc.n, 48, replace=False)
+        kinds = np.arange(len(bad)) % 8
+        nan, inf = np.float32(np.nan), np.float32(np.inf)
+        for i, k in zip(bad, kinds):
+            if k == 0:
+                sc.means[i, 0] = nan
+            elif k == 1:
+                sc.means[i, 2] = -inf
+            elif k == 2:
+                sc.log_scales[i, 1] = inf
+            elif k == 3:
+                sc.log_scales[i, 0] = -inf
+            elif k == 4:
+                sc.opacity_logits[i] = nan
+            elif k == 5:
+                sc.opacity_logits[i] = inf
+            elif k == 6:
+                sc.quats[i] = 0.0
+            else:
+                sc.quats[i, 3] = nan
+        sc.bad = np.sort(bad)
+        return sc
     raise KeyError(name)
 
 
@@ -72,7 +111,7 @@ def _case(name, mode="gather", tile=None):
 
 
 SCENES = ["tiny", "small", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3", "random_sh1", "random_sh2",
-          "random_sh3_tile16"]
+          "random_sh3_tile16", "rotated_sh3", "opaque_sh3", "nonfinite_sh3"]
 
 
 @pytest.mark.parametrize("name", SCENES)
@@ -107,7 +146,8 @@ def test_tile_lists_bit_exact(name):
     assert np.array_equal(np.diff(np.append(po[order], po[-1])), gpu["tile_count"][order].astype(np.int64))
 
 
-@pytest.mark.parametrize("name", ["small_reduced", "1m_reduced", "stress_reduced", "random_sh3_tile16"])
+@pytest.mark.parametrize("name", ["small_reduced", "1m_reduced", "stress_reduced", "random_sh3_tile16",
+                                  "rotated_sh3"])
 def test_pair_keys_bound_every_hit(name):
     """Each pair's key is at most the oracle's tau (Eq. 3) at every pixel of
     its tile where the ray hits the Gaussian: the forward's early compositing
@@ -183,6 +223,27 @@ def test_backward_parity(name, mode):
     for k in GROUPS:
         e = rel_l2(gpu["grads"][k], grads[k])
         assert e <= GRAD_TOL, (k, e)
+        assert np.isfinite(gpu["grads"][k]).all(), k
+        pe = per_gaussian_err(gpu["grads"][k], grads[k])
+        assert pe <= ELEM_TOL, (k, pe)
+
+
+def test_nonfinite_parameters_culled():
+    """Gaussians with NaN or infinite means, log-scales or logits, or a
+    zero-norm or NaN quaternion, are culled on both sides: empty rectangle,
+    no pairs, zero gradients, and no NaN anywhere in the outputs."""
+    sc, o, info, ren, grads, gpu = _case("nonfinite_sh3")
+    bad = sc.bad
+    assert (info.state[bad] == oracle.STATE_CULLED_NONFINITE).all()
+    assert (gpu["rect"][bad, 0] > gpu["rect"][bad, 2]).all()
+    assert (np.diff(gpu["lt_offset"])[bad] == 0).all() and (gpu["tile_count"][bad] == 0).all()
+    assert not np.isin(gpu["pair_prim"], bad).any()
+    assert np.isfinite(gpu["image"]).all()
+    for k in GROUPS:
+        assert np.isfinite(gpu["grads"][k]).all(), k
+        assert (gpu["grads"][k][bad] == 0).all(), k
+    assert (info.state != oracle.STATE_ACTIVE).sum() >= len(bad)
+    assert (info.state == oracle.STATE_ACTIVE).sum() > 200
 
 
 @pytest.mark.parametrize("name", ["tiny", "1m_reduced", "random_sh3"])
@@ -248,8 +309,14 @@ STORAGE_BARS = {("gather", "half"): 2.1e-3, ("hybrid", "half"): 6e-4, ("scatter"
                 ("gather", "fixed16"): 2.9e-4, ("hybrid", "fixed16"): 1e-4, ("scatter", "fixed16"): 2.9e-4}
 
 
+# The bars hold for the workload-like scenes.  The nearly opaque scene is left
+# out: a quantised L enters the colour behind a hit divided by 1 - alpha,
+# which reaches ~1e-8 there, so no storage-only bar applies to it.
+STORAGE_SCENES = [s for s in SCENES if s != "opaque_sh3"]
+
+
 @pytest.mark.parametrize("mode,prec", sorted(STORAGE_BARS))
-@pytest.mark.parametrize("name", SCENES)
+@pytest.mark.parametrize("name", STORAGE_SCENES)
 def test_backward_reduced_storage(name, mode, prec):
     sc, o, info, ren, grads, ref = _case(name, mode)
     gpu = run_gpu(sc, mode=mode, precision=prec)

@@ -140,3 +140,48 @@ def test_lt_entry_bytes(lib):
     st.lt_precision = 7
     assert lib.gart_lt_entry_bytes(ctypes.byref(st)) == 0
     assert lib.gart_lt_entry_bytes(None) == 0
+
+
+@pytest.mark.parametrize("call", ["tile_map", "forward", "backward"])
+@pytest.mark.parametrize("change", ["tile", "width", "height"])
+def test_frame_geometry_checked_on_host(lib, call, change):
+    """A frame sized by gart_bounds for one image and tile size is refused by
+    later calls that describe another (the pixel state, tile ranges and hit
+    lists are indexed with them): INVALID_ARG before anything is launched.
+    The frame's stage is set by hand, so no GPU is involved."""
+    cam, st, g, f = _structs(tile=8, w=16, h=16)
+    f.stage = 3
+    f.width, f.height, f.tile = 16, 16, 8
+    f.tiles_x = f.tiles_y = 2
+    f.lt_format = 0
+    if change == "tile":
+        st.tile = 16
+    elif change == "width":
+        cam.width = 17  # still two 8-pixel tile columns, but a wider pixel state
+    else:
+        cam.height = 15
+    dl = ctypes.c_float(0)
+    if call == "tile_map":
+        r = lib.gart_build_tile_map(ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f), None)
+    elif call == "forward":
+        r = lib.gart_forward(ctypes.byref(g), ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f),
+                             ctypes.byref(dl), None)
+    else:
+        r = lib.gart_backward(ctypes.byref(g), ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f),
+                              ctypes.byref(dl), None, None, None, None, None, None)
+    assert r == -1, (call, change, lib.gart_last_error())
+    msg = lib.gart_last_error().decode()
+    assert "gart_bounds" in msg or "tile grid" in msg, msg
+
+
+def test_frame_status_query_validated_on_host(lib):
+    """gart_frame_status (the forward's GART_FRAME_* status word) refuses a
+    NULL frame or output, and a frame the forward has not run on."""
+    cam, st, g, f = _structs()
+    v = ctypes.c_uint32(7)
+    assert lib.gart_frame_status(None, ctypes.byref(v), None) == -1
+    assert lib.gart_frame_status(ctypes.byref(f), None, None) == -1
+    f.stage = 2
+    assert lib.gart_frame_status(ctypes.byref(f), ctypes.byref(v), None) == -1
+    assert "gart_forward" in lib.gart_last_error().decode()
+    assert v.value == 7
