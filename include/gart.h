@@ -274,6 +274,28 @@ size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, c
 gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
                         gart_frame* frame, int64_t* lt_entries_host, int64_t* pair_count_host, void* stream);
 
+/* Largest n gart_bounds_noalloc serves (2^25 Gaussians). */
+#define GART_BOUNDS_NOALLOC_MAX_N (INT64_C(1) << 25)
+
+/* gart_bounds for callers that cannot allocate device memory (code under
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same computation and outputs as gart_bounds, bit for bit, but the step's
+ * scratch (block partial sums, prefix-sum temporaries and the totals) is a
+ * 4 MiB array the library holds as a static device variable, one copy per
+ * GPU, kept until the process ends.  frame->scratch is neither read nor
+ * written and may be NULL (the later calls still need it).  Calls no
+ * hipMalloc, hipFree or other allocating routine; synchronises `stream`
+ * once, as gart_bounds does.
+ * Every call on one GPU shares that GPU's copy of the array: calls that
+ * overlap in time on one GPU (from several streams or threads) race and
+ * must be serialised by the caller.  Nothing in the array needs to start at
+ * zero (each call writes every word it reads first).
+ * Errors: as gart_bounds; INVALID_ARG (nothing launched) if
+ * g->n > GART_BOUNDS_NOALLOC_MAX_N. */
+gart_status gart_bounds_noalloc(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                                gart_frame* frame, int64_t* lt_entries_host, int64_t* pair_count_host,
+                                void* stream);
+
 /* Tile-primitive mapping (Sec. 4.3 "reverse tile mapping").
  * Emits one (tile, Gaussian) pair per tile that a rectangle overlaps and
  * radix-sorts the pairs by tile id, then builds tile_range (the tile offset

@@ -7,11 +7,15 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/gart.h"
 #include "ops.h"
 
 using namespace gart;
+
+// Scratch of gart_bounds_noalloc (see gart.h): 4 MiB per GPU.
+static __device__ __align__(256) unsigned char scratch[size_t(4) << 20];
 
 namespace {
 
@@ -236,6 +240,47 @@ gart_status run_bounds(const gart_gaussians* g, const gart_camera* camera, const
   return GART_OK;
 }
 
+// ---- allocation-free bounds (gart_bounds_noalloc) ----
+// The scratch of the bounds step held by the library itself, one copy per
+// GPU for the life of the process, so that callers that cannot allocate
+// device memory need not bring any.  Host code never uses the array's name
+// as an address: each device's address comes from hipGetSymbolAddress.
+struct StaticLayout {
+  size_t scan_tmp, totals, partials, total;
+};
+
+StaticLayout static_layout(int64_t n) {
+  StaticLayout L{};
+  const int64_t nn = std::max<int64_t>(n, 1);
+  L.scan_tmp = 0;
+  L.totals = align_up(scan_tmp_bytes(nn + 1));
+  L.partials = L.totals + align_up(64);
+  L.total = L.partials + align_up(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
+  return L;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+void* g_static_ptr[kMaxDevices] = {};
+
+// Device address of this GPU's copy of the static scratch, looked up once per
+// device with that device current.
+hipError_t static_scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (g_static_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_static_ptr[dev] = p;
+  }
+  *out = g_static_ptr[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -335,6 +380,25 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   S.scan_tmp = at<void>(f->scratch, L.scan_tmp);
   S.totals = at<unsigned long long>(f->scratch, L.totals);
   S.partials = at<unsigned long long>(f->scratch, L.partials);
+  return run_bounds(g, camera, settings, f, lt_entries_host, pair_count_host, static_cast<hipStream_t>(stream), S);
+}
+
+gart_status gart_bounds_noalloc(const gart_gaussians* g, const gart_camera* camera, const gart_settings* settings,
+                                gart_frame* f, int64_t* lt_entries_host, int64_t* pair_count_host, void* stream) {
+  g_err[0] = 0;
+  gart_status st;
+  if ((st = check_bounds_args(g, camera, settings, f)) != GART_OK) return st;
+  GART_REQUIRE(g->n <= GART_BOUNDS_NOALLOC_MAX_N,
+               "n = %lld exceeds the %lld Gaussians the library's static scratch serves (use gart_bounds)",
+               (long long)g->n, (long long)GART_BOUNDS_NOALLOC_MAX_N);
+  const StaticLayout SL = static_layout(g->n);
+  GART_REQUIRE(SL.total <= sizeof(scratch), "static scratch of %zu bytes < required %zu", sizeof(scratch), SL.total);
+  char* base = nullptr;
+  GART_HIP(static_scratch_ptr(reinterpret_cast<void**>(&base)));
+  BoundsScratch S;
+  S.scan_tmp = base + SL.scan_tmp;
+  S.totals = reinterpret_cast<unsigned long long*>(base + SL.totals);
+  S.partials = reinterpret_cast<unsigned long long*>(base + SL.partials);
   return run_bounds(g, camera, settings, f, lt_entries_host, pair_count_host, static_cast<hipStream_t>(stream), S);
 }
 

@@ -109,6 +109,8 @@ def lib():
         L.gart_lt_entry_bytes.argtypes = [_P]
         L.gart_bounds.restype = ctypes.c_int
         L.gart_bounds.argtypes = [_P, _P, _P, _P, _P, _P, _P]
+        L.gart_bounds_noalloc.restype = ctypes.c_int
+        L.gart_bounds_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _P]
         L.gart_build_tile_map.restype = ctypes.c_int
         L.gart_build_tile_map.argtypes = [_P, _P, _P, _P]
         L.gart_forward.restype = ctypes.c_int
@@ -366,6 +368,25 @@ def gart_bounds(g: Gaussians, camera: gart_camera, settings: gart_settings, fram
     if st == GART_ERR_CAPACITY:
         raise GartCapacityError("gart_bounds", lib().gart_last_error().decode(), lt.value, pc.value)
     _check(st, "gart_bounds")
+    return lt.value, pc.value
+
+
+BOUNDS_NOALLOC_MAX_N = 1 << 25
+
+
+def gart_bounds_noalloc(g: Gaussians, camera: gart_camera, settings: gart_settings, frame: Frame, stream=None):
+    """gart_bounds with the library's static scratch instead of the frame's
+    (for callers that cannot allocate).  Returns (lt_entries, pair_count);
+    raises GartCapacityError if the frame's buffers are too small."""
+    gs = g.c_struct()
+    fs = frame.c_struct()
+    lt = ctypes.c_int64(0)
+    pc = ctypes.c_int64(0)
+    st = lib().gart_bounds_noalloc(ctypes.byref(gs), ctypes.byref(camera), ctypes.byref(settings),
+                                   ctypes.byref(fs), ctypes.byref(lt), ctypes.byref(pc), _stream(stream))
+    if st == GART_ERR_CAPACITY:
+        raise GartCapacityError("gart_bounds_noalloc", lib().gart_last_error().decode(), lt.value, pc.value)
+    _check(st, "gart_bounds_noalloc")
     return lt.value, pc.value
 
 
