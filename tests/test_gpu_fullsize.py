@@ -1,9 +1,10 @@
 """GPU parity at the full workload sizes, in the launch configuration that
-bench.py times (8x8 tiles, gather backward), on outputs the oracle computes
-one by one: every rectangle, a sample of tiles' Gaussian sets, a sample of
-pixels, and the complete gradients of a sample of Gaussians (the oracle
-renders every pixel of those Gaussians' rectangles, so their gradients are
-exact).
+bench.py times (8x8 tiles; the gather backward on every workload, and at 1M
+also every other backward mode and intermediate-buffer layout bench.py
+times), on outputs the oracle computes one by one: every rectangle, a sample
+of tiles' Gaussian sets, a sample of pixels, and the complete gradients of a
+sample of Gaussians (the oracle renders every pixel of those Gaussians'
+rectangles, so their gradients are exact).
 
 The upstream gradient is the generator's +-1 field (the distribution of an
 L1 loss gradient); rendering the perturbed-means target at these sizes on
@@ -13,7 +14,7 @@ import numpy as np
 import pytest
 
 import oracle
-from helpers import rel_l2, run_gpu
+from helpers import per_gaussian_err, rel_l2, run_gpu
 from paper_2608_17298_amd.scenes import make_scene
 
 pytestmark = pytest.mark.gpu
@@ -32,40 +33,24 @@ def _brute_tile(rect, state, t, W, H, ts):
     return np.nonzero(hit)[0]
 
 
-@pytest.mark.parametrize("name,max_area", [("1m", 2500), ("4m", 2500), ("stress", 2500)])
-def test_fullsize_sampled(name, max_area):
+ELEM_TOL = 1e-3  # per-Gaussian bar, as in test_gpu_parity
+# reduced-precision layouts: the bars of test_gpu_parity's storage test
+STORAGE_BARS = {("gather", "half"): 2.1e-3, ("gather", "fixed16"): 2.9e-4, ("hybrid", "fixed16"): 1e-4}
+
+_ref = {}
+
+
+def _oracle_reference(name, max_area=2500):
+    """Oracle outputs for the sampled checks of one workload (computed once)."""
+    if name in _ref:
+        return _ref[name]
     rng = np.random.default_rng(2608)
     sc = make_scene(name)
-    print(f"[{name}] N={sc.n} {sc.camera.width}x{sc.camera.height}", flush=True)
-    gpu = run_gpu(sc, mode="gather")
     o = oracle.OracleScene(sc)
     info = o.prim_info()
-    W, H, ts = o.W, o.H, sc.tile
-
-    # Rectangles and primitive offsets, every Gaussian.
-    assert np.array_equal(gpu["rect"], info.rect)
-    assert np.array_equal(np.diff(gpu["lt_offset"]), info.area)
-
-    # Gaussian set of sampled tiles.
-    n_tiles = len(gpu["tile_range"]) - 1
-    tr = gpu["tile_range"]
-    for t in rng.choice(n_tiles, 150, replace=False):
-        got = np.sort(gpu["pair_prim"][tr[t]:tr[t + 1]].astype(np.int64))
-        assert np.array_equal(got, _brute_tile(info.rect, info.state, t, W, H, ts)), t
-
-    # Sampled pixels: colour, composited count and end marker.
+    W, H = o.W, o.H
     pix = np.sort(rng.choice(W * H, 3000, replace=False))
     ren = o.render(pix)
-    ok = ren["margin"] >= AMBIG
-    img = gpu["image"].reshape(-1, 3)[pix]
-    assert np.abs(img - ren["color"])[ok].max() <= PIX_TOL
-    assert np.array_equal(gpu["n_hits"][pix][ok], ren["n_included"][ok])
-    term = ok & np.isfinite(ren["tau_end"])
-    assert np.array_equal(gpu["id_end"][pix][term], ren["id_end"][term])
-
-    # Complete gradients of sampled Gaussians with modest rectangles, drawn
-    # from those the oracle composites at one of the sampled pixels (in a
-    # deep scene most Gaussians are hidden and have zero gradient).
     _, prim, _, _ = o.records(pix, ren["n_included"])
     vis = np.unique(prim)
     cand = vis[(info.area[vis] >= 30) & (info.area[vis] <= max_area)]
@@ -80,9 +65,69 @@ def test_fullsize_sampled(name, max_area):
     print(f"[{name}] oracle backward over {len(pixels)} pixels", flush=True)
     ref = o.backward(sc.dl_dimage, pixels=pixels)
     assert (np.abs(ref["means"][sel]).sum(axis=1) > 0).all()
+    _ref[name] = (sc, o, info, rng, pix, ren, sel, ref)
+    return _ref[name]
+
+
+def _check_sampled_grads(gpu, sel, ref, tol):
     for k in GROUPS:
         e = rel_l2(gpu["grads"][k][sel], ref[k][sel])
-        assert e <= GRAD_TOL, (k, e)
+        assert e <= tol, (k, e)
+        assert np.isfinite(gpu["grads"][k]).all(), k
+        if tol <= GRAD_TOL:
+            pe = per_gaussian_err(gpu["grads"][k][sel], ref[k][sel])
+            assert pe <= ELEM_TOL, (k, pe)
+
+
+@pytest.mark.parametrize("name", ["1m", "4m", "stress"])
+def test_fullsize_sampled(name):
+    sc, o, info, rng, pix, ren, sel, ref = _oracle_reference(name)
+    print(f"[{name}] N={sc.n} {sc.camera.width}x{sc.camera.height}", flush=True)
+    gpu = run_gpu(sc, mode="gather")
+    W, H, ts = o.W, o.H, sc.tile
+
+    # Rectangles and primitive offsets, every Gaussian.
+    assert np.array_equal(gpu["rect"], info.rect)
+    assert np.array_equal(np.diff(gpu["lt_offset"]), info.area)
+
+    # Gaussian set of sampled tiles.
+    n_tiles = len(gpu["tile_range"]) - 1
+    tr = gpu["tile_range"]
+    for t in rng.choice(n_tiles, 150, replace=False):
+        got = np.sort(gpu["pair_prim"][tr[t]:tr[t + 1]].astype(np.int64))
+        assert np.array_equal(got, _brute_tile(info.rect, info.state, t, W, H, ts)), t
+
+    # Sampled pixels: colour, composited count and end marker.
+    ok = ren["margin"] >= AMBIG
+    img = gpu["image"].reshape(-1, 3)[pix]
+    assert np.abs(img - ren["color"])[ok].max() <= PIX_TOL
+    assert np.array_equal(gpu["n_hits"][pix][ok], ren["n_included"][ok])
+    term = ok & np.isfinite(ren["tau_end"])
+    assert np.array_equal(gpu["id_end"][pix][term], ren["id_end"][term])
+
+    # Complete gradients of sampled Gaussians with modest rectangles, drawn
+    # from those the oracle composites at one of the sampled pixels (in a
+    # deep scene most Gaussians are hidden and have zero gradient).
+    _check_sampled_grads(gpu, sel, ref, GRAD_TOL)
+
+
+@pytest.mark.parametrize("mode,prec", [("gather_wave", "full"), ("gather_atomic", "full"), ("scatter", "full"),
+                                       ("hybrid", "full"), ("gather", "half"), ("gather", "fixed16"),
+                                       ("hybrid", "fixed16")])
+def test_fullsize_1m_every_timed_variant(mode, prec):
+    """The 1M workload in every backward mode and intermediate-buffer layout
+    that bench.py times: sampled pixels (the image does not depend on the
+    mode or layout) and the complete gradients of the 24 sampled Gaussians,
+    at the full-precision bars (reduced layouts: their storage bars)."""
+    sc, o, info, rng, pix, ren, sel, ref = _oracle_reference("1m")
+    print(f"[1m] mode {mode}, layout {prec}", flush=True)
+    gpu = run_gpu(sc, mode=mode, precision=prec)
+    ok = ren["margin"] >= AMBIG
+    img = gpu["image"].reshape(-1, 3)[pix]
+    assert np.abs(img - ren["color"])[ok].max() <= PIX_TOL
+    assert np.array_equal(gpu["n_hits"][pix][ok], ren["n_included"][ok])
+    tol = GRAD_TOL if prec == "full" else STORAGE_BARS[(mode, prec)]
+    _check_sampled_grads(gpu, sel, ref, tol)
 
 
 def test_tile_map_past_two_level_scan():
