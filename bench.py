@@ -28,33 +28,46 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
-# Vector ALU peak from the unit counts: 256 CUs x 4 SIMDs x 16 lanes x 2 flops
-# (FMA) x 2.4 GHz = 78.6 TFLOP/s, for fp64 and for fp32 without packed
-# instructions (the library is built without them; the 157.3 TFLOP/s fp32
-# figure counts two packed operations per lane).
-FP32_PEAK_TFLOPS = 78.6
-FP64_PEAK_TFLOPS = 78.6
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+FP32_PEAK_TFLOPS = 157.3       # MI355X vector fp32, published
+FP64_PEAK_TFLOPS = 78.6        # MI355X vector fp64, published
 
-# Algorithmic cost model (per unit of work).
-F64_PER_TEST = 40              # ray/Gaussian max-response test in fp64 (W d, two dots, tau, x_g, D2, compare)
-F64_PER_HIT_BWD = 45           # gather: x_g and D2 of a composited hit in fp64 (no decision)
-GEOM_BYTES = 128 + 16 + 8 + 4  # per staged pair in the forward: fp64 geometry row, rect, O_prim, pair index
-UNIT_BYTES = 104 + 8 + 16 + 8 + 8  # per gather unit: W and o_g, sigma, rect, O_prim, pair offset
+# Algorithmic cost per unit of work: what the method must move or compute,
+# independent of how the kernels do it.
+#   composited hit, backward: 16 B (L,T) read; 12K + 90 fp32 flops
+#   composited hit, forward: 16 B (L,T) write; 6K fp32 flops (colour)
+#   (pixel, Gaussian) ray test (fwd and bwd): 45 fp64 flops
+#   pixel: 40 B read by the backward (dL/dC 12, C 12, end marker 16); 12 B image written by the forward
+#   Gaussian: 4P B of parameters read by the backward, 4P B of gradients written by the reduction
+#             (P = 11 + 3K values), ~200 fp64 flops of chain rule
+LT_BYTES_PER_HIT = 16
+PIXEL_BYTES_BWD = 40
+PIXEL_BYTES_FWD = 12
+F64_PER_TEST = 45
+F64_PER_CHAIN = 200
+
+
+def f32_per_hit_bwd(K):
+    return 12 * K + 90
+
+
+def f32_per_hit_fwd(K):
+    return 6 * K
+
+
+def param_bytes(K):
+    return 4 * (11 + 3 * K)
+
+
+# Implementation cost model (the bytes these kernels' designs must move, as
+# opposed to the algorithmic figures above), reported beside them.
+IMPL_GEOM_BYTES = 128 + 16 + 8 + 4  # per staged pair in the forward: fp64 geometry row, rect, O_prim, pair index
+IMPL_UNIT_BYTES = 104 + 8 + 16 + 8 + 8  # per gather unit: W and o_g, sigma, rect, O_prim, pair offset
 
 
 ALL_MODES = ("gather", "gather_wave", "gather_atomic", "scatter", "hybrid")
 # backward mode + intermediate-buffer precision pairs timed beside the default
 STORAGE_VARIANTS = (("gather", "fixed16"), ("gather", "half"), ("hybrid", "fixed16"))
-
-
-def f32_per_hit_bwd(K):
-    # colour 6K, per-hit gradient terms ~25, AW products (9 + 3K), AW accumulations (10 + 3K)
-    return 6 * K + 25 + (9 + 3 * K) + (10 + 3 * K)
-
-
-def f32_per_hit_fwd(K):
-    return 6 * K + 10  # colour, compositing (the exp and T update counted as fp64)
 
 
 def parse():
@@ -182,6 +195,7 @@ def main():
         counts[mode] = frame.counters.cpu().numpy().astype(np.int64)
     frame.counters = None
     c = counts[args.mode]
+    vram = frame_vram(frame, sc)
     hits = int(c[gart.CNT_FWD_HITS])
 
     def make_events(n):
@@ -231,6 +245,10 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     ms_per_step = 1e3 * wall / args.steps
+    fwd_status = gart.gart_frame_status(frame)
+    if fwd_status != 0:
+        print(f"bench.py: forward status {fwd_status:#x} (incomplete trace)", file=sys.stderr)
+        sys.exit(3)
 
     def avg(fn):
         return float(np.mean([fn(cl, kr) for cl, kr in per]))
@@ -242,58 +260,71 @@ def main():
         pair_sort=avg(lambda cl, kr: ms(kr[0], kr[1])), forward_trace=avg(lambda cl, kr: ms(kr[2], kr[3])),
         backward_main=avg(lambda cl, kr: ms(kr[4], kr[5])), reduce_chain=avg(lambda cl, kr: ms(kr[6], kr[7])))
 
-    # Algorithmic work of the two dominant kernels.
+    # Work of the dominant kernels per launch, from the counting run's unit
+    # counts and the algorithmic costs per unit.
     npix = W * H
     AW = 10 + 3 * K
-    AS = (AW + 3) & ~3
+    AS = 16 if AW <= 16 else (AW + 31) // 32 * 32  # partial-row stride in floats (whole 128-byte lines)
     bwd_tests, bwd_hits = int(c[gart.CNT_BWD_TESTS]), int(c[gart.CNT_BWD_HITS])
     bwd_pairs, bwd_active = int(c[gart.CNT_BWD_PAIRS]), int(c[gart.CNT_BWD_ACTIVE])
     fwd_tests = int(c[gart.CNT_FWD_TESTS])
-    # gather: per composited hit its (L,T) entry and hit-list word; per visited
-    # pair its index and depth bound; per (pair, group) unit with hits the
-    # Gaussian's geometry and SH, one partial row and its flag; per pixel the
-    # upstream gradient and pixel state.  forward: per composited hit the
-    # (L,T) entry and hit-list word written; per pair of the visited prefix
-    # (the list up to the tile's last ray end) its geometry row; SH once per
-    # (tile, Gaussian) with hits; per pixel the image and state.
+    N = sc.n
     work = {
         "backward_main": dict(
-            bytes=20 * bwd_hits + 12 * bwd_pairs + bwd_active * (UNIT_BYTES + 12 * K + 4 * AS + 1) + npix * (12 + 32),
-            f64=F64_PER_TEST * bwd_tests + F64_PER_HIT_BWD * bwd_hits, f32=f32_per_hit_bwd(K) * bwd_hits),
+            bytes=LT_BYTES_PER_HIT * bwd_hits + PIXEL_BYTES_BWD * npix + param_bytes(K) * N,
+            f64=F64_PER_TEST * bwd_tests, f32=f32_per_hit_bwd(K) * bwd_hits),
+        "backward": dict(
+            bytes=LT_BYTES_PER_HIT * bwd_hits + PIXEL_BYTES_BWD * npix + 2 * param_bytes(K) * N,
+            f64=F64_PER_TEST * bwd_tests + F64_PER_CHAIN * N, f32=f32_per_hit_bwd(K) * bwd_hits),
         "forward_trace": dict(
-            bytes=20 * hits + bwd_pairs * GEOM_BYTES + bwd_active * 12 * K + npix * (12 + 32),
-            f64=F64_PER_TEST * fwd_tests + 30 * hits, f32=f32_per_hit_fwd(K) * hits),
+            bytes=LT_BYTES_PER_HIT * hits + PIXEL_BYTES_FWD * npix,
+            f64=F64_PER_TEST * fwd_tests, f32=f32_per_hit_fwd(K) * hits),
     }
+    # bytes the kernels' own designs move (staged geometry, SH, partial rows,
+    # hit lists), for comparison with the algorithmic figures
+    impl_bytes = {
+        "backward_main": 20 * bwd_hits + 12 * bwd_pairs + bwd_active * (IMPL_UNIT_BYTES + 12 * K + 4 * AS + 1)
+        + npix * (12 + 32),
+        "forward_trace": 20 * hits + bwd_pairs * IMPL_GEOM_BYTES + bwd_active * 12 * K + npix * (12 + 32),
+    }
+    times_ms = {"backward_main": kern_ms["backward_main"], "backward": call_ms["backward"],
+                "forward_trace": kern_ms["forward_trace"]}
 
     def roofline(name):
         w = work[name]
-        t = kern_ms[name] * 1e-3
+        t = times_ms[name] * 1e-3
         t_hbm = w["bytes"] / (HBM_PEAK_GBS * 1e9)
         t_alu = w["f32"] / (FP32_PEAK_TFLOPS * 1e12) + w["f64"] / (FP64_PEAK_TFLOPS * 1e12)
+        common = dict(algorithmic_bytes=w["bytes"], f32_flops=w["f32"], f64_flops=w["f64"],
+                      time_ms=round(times_ms[name], 4), roofline_ms=round(1e3 * max(t_hbm, t_alu), 4))
         if t_hbm >= t_alu:
             achieved = w["bytes"] / t / 1e9
             return dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                        frac=round(achieved / HBM_PEAK_GBS, 4))
+                        frac=round(achieved / HBM_PEAK_GBS, 4), **common)
         flops = w["f32"] + w["f64"]
-        peak = flops / t_alu / 1e12  # mix-weighted ALU peak for this kernel's fp32/fp64 split
+        peak = flops / t_alu / 1e12  # the published fp32 / fp64 peaks weighted by this kernel's mix
         achieved = flops / t / 1e12
         return dict(bound="alu", achieved=round(achieved, 3), peak=round(peak, 1), unit="TFLOP/s",
-                    frac=round(achieved / peak, 4), f32_flops=w["f32"], f64_flops=w["f64"],
-                    hbm_bytes_algorithmic=w["bytes"])
+                    frac=round(achieved / peak, 4), **common)
 
     def with_counters(name):
         r = roofline(name)
-        rec = recorded_profile("gather" if name == "backward_main" else "forward", args.workload)
+        prof = {"backward_main": "gather", "forward_trace": "forward"}.get(name)
+        rec = recorded_profile(prof, args.workload) if prof else {}
         r["traffic"] = rec.get("hbm_bytes_per_launch")
         vb = rec.get("valu_busy_pct")
         r["valu_busy"] = None if vb is None else round(vb / 100.0, 4)
         vu = rec.get("valu_utilization_pct")
         r["valu_utilization"] = None if vu is None else round(vu / 100.0, 4)
+        if name in impl_bytes:
+            r["implementation_bytes"] = impl_bytes[name]
         return r
 
-    dominant = max(("forward_trace", "backward_main"), key=lambda k: kern_ms[k])
-    roof = with_counters(dominant)
-    roof["kernel"] = "gather_kernel" if dominant == "backward_main" else "forward_kernel"
+    # Headline: the gather backward's main kernel, whose throughput `value`
+    # measures and whose roofline fraction the target is set on; the whole
+    # backward (with the reduction) and the forward are reported beside it.
+    roof = with_counters("backward_main")
+    roof["kernel"] = "gather_kernel"
 
     value = bwd_hits / (call_ms["backward"] * 1e-3)
 
@@ -347,6 +378,8 @@ def main():
                                f"{sc.tile}x{sc.tile} tiles", "backward_mode": args.mode,
                    "composited_hits": hits, "pairs": int(frame.pair_count), "lt_entries": int(frame.lt_entries)},
         "roofline": roof,
+        "roofline_backward_with_reduction": with_counters("backward"),
+        "roofline_forward": dict(with_counters("forward_trace"), kernel="forward_kernel"),
         "cpu_baseline": cpu,
         "call_ms": {k: round(v, 4) for k, v in call_ms.items()},
         "kernel_ms": {k: round(v, 4) for k, v in kern_ms.items()},
@@ -356,7 +389,7 @@ def main():
         "counters": {name: int(c[i]) for i, name in enumerate(
             ["fwd_hits", "fwd_tests", "fwd_rescans", "bwd_hits", "bwd_tests", "bwd_atomics", "bwd_pairs",
              "bwd_active_units", "fwd_drops", "bwd_hybrid_steps", "bwd_wave_units"])},
-        "kernels_roofline": {k: with_counters(k) for k in work},
+        "vram_bytes": vram,
         "train_step": train,
     }
     s = json.dumps(line)
@@ -364,6 +397,24 @@ def main():
     if args.out:
         with open(args.out, "w") as f:
             f.write(s + "\n")
+
+
+def frame_vram(frame, sc):
+    """Device bytes of the frame's buffers as allocated (capacities with the
+    bench's slack, scratch sized for every backward mode) and as used by this
+    workload (counts from gart_bounds)."""
+    nb = lambda t: int(t.numel() * t.element_size())
+    alloc = dict(lt=nb(frame.lt), hit_list=nb(frame.hit_list),
+                 pairs=nb(frame.pair_tile) + nb(frame.pair_prim) + nb(frame.pair_key),
+                 scratch=nb(frame.scratch),
+                 per_gaussian=nb(frame.rect) + nb(frame.lt_offset) + nb(frame.prim_geom) + nb(frame.tile_count)
+                 + nb(frame.pair_offset),
+                 pixel_state=nb(frame.pixel_state), tile_range=nb(frame.tile_range))
+    alloc["total"] = sum(alloc.values())
+    P, E, ts = frame.pair_count, frame.lt_entries, sc.tile
+    used = dict(lt=16 * E, hit_list=4 * ts * ts * P, pairs=12 * P)
+    return {"allocated": alloc, "used_by_workload": used,
+            "torch_max_allocated": int(__import__("torch").cuda.max_memory_allocated())}
 
 
 def train_timing(sc, steps, n_views):
