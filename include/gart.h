@@ -161,9 +161,14 @@ typedef struct {
   int64_t pair_capacity;  /* number of (tile, prim) pair slots allocated */
   uint32_t* pair_tile;    /* [pair_capacity] tile id of each pair, sorted ascending */
   uint32_t* pair_prim;    /* [pair_capacity] Gaussian index of each pair */
-  float* pair_key;        /* [pair_capacity] lower bound on tau (Eq. 3) of the Gaussian's maximum
-                             response along every pixel ray of the pair's tile; each tile's list is
-                             sorted ascending by it, then by Gaussian index */
+  float* pair_key;        /* [pair_capacity] lower bound on tau_q / s_q over the pixel-centre rays q of
+                             the pair's tile inside the Gaussian's rectangle, where tau_q is the depth
+                             (Eq. 3) of the Gaussian's maximum-response point (Eq. 4-5) on ray q,
+                             s_q = |R^T u_q| / (c . u_q), u_q = ((x + 1/2 - cx)/fx, (y + 1/2 - cy)/fy, 1),
+                             and c is the unit camera-space direction through the tile centre
+                             (pixel ((tx + 1/2) tile, (ty + 1/2) tile)): the depth measured along c
+                             (s_q - 1 < 2e-5 on 8x8 tiles); each tile's list is sorted ascending by
+                             it, then by Gaussian index */
   int64_t* tile_range;    /* [n_tiles+1] pairs of tile t are [tile_range[t], tile_range[t+1]) */
   /* written by gart_forward, read by gart_backward */
   int64_t lt_capacity;    /* number of intermediate entries allocated, each of
@@ -299,12 +304,13 @@ gart_status gart_bounds_noalloc(const gart_gaussians* g, const gart_camera* came
 /* Tile-primitive mapping (Sec. 4.3 "reverse tile mapping").
  * Emits one (tile, Gaussian) pair per tile that a rectangle overlaps and
  * radix-sorts the pairs by tile id, then builds tile_range (the tile offset
- * table).  Within one tile, pairs are ordered by pair_key, a conservative
- * lower bound on the ray parameter at which the Gaussian can be hit by any
- * pixel ray of that tile, rounded down to a float with min(24, 32 - tile id
- * bits) - 5 mantissa bits (0 below 2^-12, saturating below 2^20), then by
- * index; the set of Gaussians per tile is exactly the set of rectangles
- * meeting the tile.
+ * table).  Within one tile, pairs are ordered by pair_key (see gart_frame),
+ * the smallest depth along the tile's centre direction of the Gaussian's
+ * maximum-response points over the tile's pixel rays (attained at a corner
+ * of the pixel rectangle; less 1e-12 relative), rounded down to a float with
+ * min(24, 32 - tile id bits) - 5 mantissa bits (0 below 2^-12, saturating
+ * below 2^20), then by index; the set of Gaussians per tile is exactly the
+ * set of rectangles meeting the tile.
  * Requires gart_bounds on the same frame first (else INVALID_ARG). */
 gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* settings, gart_frame* frame,
                                 void* stream);

@@ -502,6 +502,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
   A.status = at<uint32_t>(f->scratch, Lf.status);
+  A.pair_count = f->pair_count;
   GART_HIP(fill_u32(A.status, 0u, 1, s));
   GART_HIP(launch_forward(A, s));
   f->lt_format = A.lt_format;

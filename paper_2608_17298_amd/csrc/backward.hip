@@ -290,7 +290,11 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
     s_ray[tid] = rr;
     *reinterpret_cast<uint4*>(&s_cg[tid][0]) = make_uint4(cq[0], cq[1], cq[2], __float_as_uint(gg[0]));
     *reinterpret_cast<float4*>(&s_cg[tid][4]) = make_float4(gg[1], gg[2], 0.0f, 0.0f);
-    double m = tend;
+    // the latest ray end in the tile's key units (a key k bounds a hit's
+    // depth on this ray by k * key_scale), rounded up
+    double cax[3];
+    tile_axis(A.cam, tx, ty, TILE, cax);
+    double m = tend / key_scale(A.cam, cax, valid ? px : 0, valid ? py : 0);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
     if (tid % 64 == 0) s_wmax[tid / 64] = m;
@@ -301,7 +305,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
   for (int w = 1; w < G; ++w) tmax = fmax(tmax, s_wmax[w]);
 
   // Only the prefix of the depth-ordered list whose depth bound lies in front
-  // of the tile's last ray end can hold composited hits.
+  // of the tile's latest ray end can hold composited hits.
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
   uint32_t nv = 0;
   for (int64_t j = beg + tid; j < end; j += NT) {
@@ -701,6 +705,9 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 
   double d[3];
   pixel_ray(A.cam, valid ? px : 0, valid ? py : 0, d);
+  double cax[3];
+  tile_axis(A.cam, tx, ty, TILE, cax);
+  const double kscale = key_scale(A.cam, cax, valid ? px : 0, valid ? py : 0);  // key -> depth bound on this ray
   float Y[K];
   sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
   uint32_t Cq[3] = {0, 0, 0};
@@ -743,7 +750,7 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
     if (!done) {
       for (int c = 0; c < nb; ++c) {
         const double* row = s_row + c * kRow;
-        if (row[14] > tend) {  // every remaining Gaussian lies behind this ray's end
+        if (row[14] * kscale > tend) {  // every remaining Gaussian lies behind this ray's end
           done = true;
           break;
         }

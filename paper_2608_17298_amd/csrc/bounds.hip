@@ -310,16 +310,24 @@ __device__ __forceinline__ float depth_code_value(uint32_t c, int bits) {
 
 // One block emits the pairs of 256 consecutive Gaussians (index order); its
 // threads stride over the block's pair slots and find their Gaussian by
-// binary search over first slots held in LDS.  Each pair gets a lower bound
-// on the depth tau of any hit of its Gaussian in its tile: the larger of the
-// Gaussian's own bound and a bound over the tile's pixel rays.  With the
-// unnormalised ray d = R^T (a, b, 1), a = (x + 1/2 - cx)/fx, b = (y + 1/2 -
-// cy)/fy, the max-response depth is tau = N |d| / D with N = n . (a, b, 1)
-// (linear), D = (a, b, 1) M (a, b, 1)^T (convex), |d| = sqrt(a^2 + b^2 + 1),
-// n = R Sigma^-1 (mu - o) and M = R Sigma^-1 R^T (R = world -> camera).  Over
-// the tile's rectangle of (a, b), N is smallest and D largest at corners and
-// |d| smallest at the point nearest (0, 0); a hit needs tau > 0, so
-// tau >= max(N_min, 0) |d|_min / D_max.
+// binary search over first slots held in LDS.  Each pair gets a lower bound on
+// the depth tau (Eq. 3) of its Gaussian's max-response point (Eq. 4-5) along
+// the pixel-centre rays of its tile that lie in the Gaussian's rectangle,
+// measured relative to the tile: the key is min over those rays q of
+// tau_q / s_q with s_q = |R^T u_q| / (c . u_q), where u_q = (a, b, 1) is the
+// camera ray of pixel q, a = (x + 1/2 - cx)/fx, b = (y + 1/2 - cy)/fy, and c
+// is the unit direction through the tile's centre (tile_axis).  s_q exceeds 1
+// by under 2e-5 on an 8x8 tile, and each kernel scales a key by its own
+// pixel's s to bound that pixel's tau.  tau_q / s_q is the depth along c of
+// the max-response point: with u' = u / (c . u), tau / s = N(u') / D(u'),
+// N(u) = -o_g . P u, D(u) = |P u|^2, P = W R^T (the world ray R^T u has
+// length |R^T u|, which cancels).  The pixel rectangle maps to a convex quadrilateral
+// of u' whose vertices are its four corner rays; N is linear and D a convex
+// quadratic on it, so for t >= 0 N - t D is concave and its minimum lies at a
+// vertex: the smallest N / D over the four corners is the exact minimum over
+// the tile's rays.  The key is that minimum less 1e-12 relative (the forward
+// evaluates tau another way), and at least the Gaussian's own bound on tau
+// divided by the largest corner s; a hit needs tau > 0.
 constexpr int kEmitGaussians = 256;
 
 __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
@@ -362,7 +370,6 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
   }
   __syncthreads();
   const uint32_t count = s_base[nr];
-  const double ifx = 1.0 / A.cam.fx, ify = 1.0 / A.cam.fy;
   for (uint32_t jr = threadIdx.x; jr < count; jr += blockDim.x) {
     int lo = 0, hi = nr - 1;  // largest k with s_base[k] <= jr
     while (lo < hi) {
@@ -375,25 +382,35 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
     const uint32_t row = q / ntx;
     const int tx = s_tile[k][0] + int(q - row * ntx), ty = s_tile[k][1] + int(row);
     const int64_t j = first + jr;
-    // the tile's pixel-centre rectangle in (a, b)
-    const double a0 = (double(tx * ts) + 0.5 - A.cam.cx) * ifx;
-    const double a1 = (double(min(A.cam.W - 1, tx * ts + ts - 1)) + 0.5 - A.cam.cx) * ifx;
-    const double b0 = (double(ty * ts) + 0.5 - A.cam.cy) * ify;
-    const double b1 = (double(min(A.cam.H - 1, ty * ts + ts - 1)) + 0.5 - A.cam.cy) * ify;
+    // corners of the pixel-centre rectangle of rect cap tile, depths along
+    // the tile's axis c
+    const int32_t* rc = A.rect + 4 * (i0 + k);
+    const double ax[2] = {(double(max(rc[0], tx * ts)) + 0.5 - A.cam.cx) / A.cam.fx,
+                          (double(min(rc[2], tx * ts + ts - 1)) + 0.5 - A.cam.cx) / A.cam.fx};
+    const double by[2] = {(double(max(rc[1], ty * ts)) + 0.5 - A.cam.cy) / A.cam.fy,
+                          (double(min(rc[3], ty * ts + ts - 1)) + 0.5 - A.cam.cy) / A.cam.fy};
+    double cax[3];
+    tile_axis(A.cam, tx, ty, ts, cax);
     const double* Q = s_q[k];
-    double nmin = __builtin_huge_val(), dmax = 0.0;
+    double kmin = __builtin_huge_val(), smax = 0.0;
 #pragma unroll
     for (int corner = 0; corner < 4; ++corner) {
-      const double a = (corner & 1) ? a1 : a0, b = (corner & 2) ? b1 : b0;
-      nmin = fmin(nmin, fma(Q[6], a, fma(Q[7], b, Q[8])));
+      const double a = ax[corner & 1], b = by[corner >> 1];
+      const double N = fma(Q[6], a, fma(Q[7], b, Q[8]));
       const double D = fma(a, fma(Q[0], a, 2.0 * fma(Q[1], b, Q[2])), fma(b, fma(Q[3], b, 2.0 * Q[4]), Q[5]));
-      dmax = fmax(dmax, D);
+      const double cu = fma(cax[0], a, fma(cax[1], b, cax[2]));  // c . u
+      kmin = fmin(kmin, N * cu / D);
+      double w2 = 0.0;  // |R^T u|^2
+#pragma unroll
+      for (int r = 0; r < 3; ++r) {
+        const double wr = fma(A.cam.Rt[3 * r], a, fma(A.cam.Rt[3 * r + 1], b, A.cam.Rt[3 * r + 2]));
+        w2 = fma(wr, wr, w2);
+      }
+      smax = fmax(smax, sqrt(w2) / cu);
     }
-    const double am = (a0 <= 0.0 && a1 >= 0.0) ? 0.0 : fmin(fabs(a0), fabs(a1));
-    const double bm = (b0 <= 0.0 && b1 >= 0.0) ? 0.0 : fmin(fabs(b0), fabs(b1));
-    double tk = nmin > 0.0 ? nmin * sqrt(fma(am, am, fma(bm, bm, 1.0))) / dmax : 0.0;
-    tk -= 1e-12 * tk;  // rounding of the bound's fp64 evaluation
-    const double bound = fmax(Q[9], tk);
+    const double tk = kmin > 0.0 ? kmin - 1e-12 * kmin : 0.0;
+    const double own = Q[9] / smax * (1.0 - 1e-12);
+    const double bound = fmax(own, tk);
     A.keys[j] = (uint32_t(ty * A.tiles_x + tx) << A.key_bits) | depth_code(bound, A.key_bits);
     A.vals[j] = uint32_t(i0 + k);
   }

@@ -17,8 +17,8 @@ namespace gart {
 
 constexpr int kGeomStride = 16;  // doubles per Gaussian in prim_geom
 // prim_geom layout (double): [0..8] W = S^-1 R^T row-major, [9..11] o_g =
-// W (o - mu), [12] squared clamp radius D2c, [13] opacity sigma, [14] depth
-// lower bound (the float sort key, widened), [15] 1 - sigma = sigmoid(-logit)
+// W (o - mu), [12] squared clamp radius D2c, [13] opacity sigma, [14] lower
+// bound on the depth tau of any hit, [15] 1 - sigma = sigmoid(-logit)
 // (so that 1 - alpha keeps its precision for nearly opaque Gaussians).
 constexpr int kGeoW = 0, kGeoOg = 9, kGeoD2c = 12, kGeoSigma = 13, kGeoKey = 14, kGeoOneMinusSigma = 15;
 
@@ -55,6 +55,35 @@ __device__ __forceinline__ void pixel_ray(const CamParams& c, int px, int py, do
   const double inv = 1.0 / sqrt(fma(v[0], v[0], fma(v[1], v[1], v[2] * v[2])));
 #pragma unroll
   for (int k = 0; k < 3; ++k) d[k] = v[k] * inv;
+}
+
+// Unit camera-space direction c through the centre of tile (tx, ty) (its
+// pixel coordinates ((tx + 1/2) ts, (ty + 1/2) ts)).  The tile's list keys are
+// depths measured along c.
+__device__ __forceinline__ void tile_axis(const CamParams& cam, int tx, int ty, int ts, double c[3]) {
+  const double a = (double(tx * ts) + 0.5 * ts - cam.cx) / cam.fx;
+  const double b = (double(ty * ts) + 0.5 * ts - cam.cy) / cam.fy;
+  const double inv = 1.0 / sqrt(fma(a, a, fma(b, b, 1.0)));
+  c[0] = a * inv;
+  c[1] = b * inv;
+  c[2] = inv;
+}
+
+// Scale s = |R^T u| / (c . u) of the camera ray u = (a, b, 1) of pixel
+// (px, py) against its tile's axis c (|R^T u| is the length of the world ray
+// vector the trace normalises, so the identity below holds for any rotation
+// matrix as given), lowered by 2^-40 against rounding: a list key k bounds
+// the depth of a hit on this pixel's ray by tau >= k s.
+__device__ __forceinline__ double key_scale(const CamParams& cam, const double c[3], int px, int py) {
+  const double a = (double(px) + 0.5 - cam.cx) / cam.fx;
+  const double b = (double(py) + 0.5 - cam.cy) / cam.fy;
+  double w2 = 0.0;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const double wk = fma(cam.Rt[3 * k], a, fma(cam.Rt[3 * k + 1], b, cam.Rt[3 * k + 2]));
+    w2 = fma(wk, wk, w2);
+  }
+  return sqrt(w2) / fma(c[0], a, fma(c[1], b, c[2])) * (1.0 - 0x1p-40);
 }
 
 // Max-response point of a Gaussian on the ray o + tau d (Eq. 4-5) in the

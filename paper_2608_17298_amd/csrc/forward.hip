@@ -2,14 +2,18 @@
 // intermediate buffer in primitive-major order (Sec. 4.3, Eq. 16).
 //
 // One workgroup per tile, one lane per pixel.  The tile's Gaussian list is
-// ordered by a conservative lower bound on the depth at which each Gaussian
-// can be hit, so a lane can stream it front to back with a small sorted hit
-// buffer held in registers: a buffered hit is final -- and is composited --
-// as soon as its depth is below the lower bound of the next Gaussian in the
-// list.  The result is exactly the (tau, index) order.  If the buffer
-// overflows, the largest hits are dropped and the lane later rescans the
-// list from the first Gaussian it dropped, skipping hits already
-// composited; compositing stops once the transmittance falls below t_min.
+// ordered by a lower bound on the depth at which each Gaussian can be hit by
+// a pixel ray of the tile, so a lane can stream it front to back with a small
+// sorted buffer of pending hits: a buffered hit is final -- and is composited
+// -- as soon as its depth is below the bound of the next Gaussian in the list.
+// The result is exactly the (tau, index) order.  The buffer is a ring of KB
+// entries per lane in LDS, laid out [slot][lane], so the lanes of a wave
+// touch consecutive words whatever slot each is at (no bank conflicts); a new
+// hit is inserted from the tail, which with tight bounds is nearly always an
+// append.  If a ring overflows, its largest hits are dropped and the lane
+// later rescans the list from the first Gaussian it dropped, skipping hits
+// already composited; compositing stops once the transmittance falls below
+// t_min.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -20,43 +24,46 @@
 namespace gart {
 namespace {
 
-#ifndef GART_FWD_KB
-#define GART_FWD_KB 14
-#endif
 #ifndef GART_FWD_FLUSH
-#define GART_FWD_FLUSH 16
+#define GART_FWD_FLUSH 8
 #endif
 #ifndef GART_FWD_BATCH
-#define GART_FWD_BATCH 256
+#define GART_FWD_BATCH 16
 #endif
-// Minimum waves per SIMD asked of the register allocator (default: none).
-#ifdef GART_FWD_WAVES
-#define GART_FWD_LAUNCH_BOUNDS(n) __launch_bounds__(n, GART_FWD_WAVES)
+
+constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
+// row: [0..8] W, [9..11] o_g, [12] D2c, [13] sigma, [14] depth key,
+// [15] O_prim (int64 bits), [16..17] rect (4 x int32), [18] index (uint32)
+
+// Each rescan composites at least one hit per rescanning lane, so the pass
+// count is bounded by the hits of a tile; this cap only guards against a
+// defect turning into a hang, and is reported in the frame status if reached.
+constexpr int kMaxPasses = 1 << 20;
+
+// Minimum 64-thread workgroups per CU asked of the register allocator (default: none).
+#ifdef GART_FWD_MINBLOCKS
+#define GART_FWD_LAUNCH_BOUNDS(n) __launch_bounds__(n) __attribute__((amdgpu_waves_per_eu(GART_FWD_MINBLOCKS / 4)))
 #else
 #define GART_FWD_LAUNCH_BOUNDS(n) __launch_bounds__(n)
 #endif
 
-constexpr int kRow = 20;  // doubles per staged Gaussian in LDS
-// Each rescan composites at least one hit per rescanning lane, so the pass
-// count is bounded by the hits of a tile; this cap only guards against a
-// defect turning into a hang.
-constexpr int kMaxPasses = 1 << 20;
-// row: [0..8] W, [9..11] o_g, [12] D2c, [13] sigma, [14] depth key,
-// [15] O_prim (int64 bits), [16..17] rect (4 x int32), [18] index (uint32)
-
-template <int TILE, int K, int FMT>
+template <int TILE, int K, int FMT, int KB>
 __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A) {
   constexpr int NT = TILE * TILE;
-  constexpr int KB = GART_FWD_KB;  // per-lane hit buffer (registers)
   constexpr int kFlushEvery = GART_FWD_FLUSH;
   constexpr int NB = GART_FWD_BATCH < NT ? GART_FWD_BATCH : NT;  // candidates staged per batch
   constexpr double kInf = __builtin_huge_val();
+  static_assert(KB >= 2 && (KB & (KB - 1)) == 0, "ring of a power-of-two size");
 
-  constexpr int KP = (K + 3) & ~3;  // SH basis row padded to 16 bytes
   __shared__ __align__(16) double s_row[NB * kRow];
-  __shared__ __align__(16) float s_Y[NT][KP];  // SH basis of each pixel's ray
   __shared__ float s_key[NB + 1];
   __shared__ unsigned s_restart;
+  // pending hits of each lane: depth rounded up to a float, alpha, and
+  // (list position, Gaussian index) -- 20 bytes; the exact depth is
+  // recomputed on the rare paths that need it
+  __shared__ float s_btf[KB][NT];
+  __shared__ double s_balpha[KB][NT];
+  __shared__ uint2 s_bpid[KB][NT];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
   const int tile = xcd_tile(blockIdx.x, n_tiles, A.tiles_x);
@@ -67,12 +74,13 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
 
   double d[3];
   pixel_ray(A.cam, valid ? px : 0, valid ? py : 0, d);
-  {
-    float Y[K];
-    sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
-#pragma unroll
-    for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
-  }
+  // the tile's list keys are depths along the tile's axis; key k bounds the
+  // depth of a hit on this pixel's ray by k * kscale
+  double cax[3];
+  tile_axis(A.cam, tx, ty, TILE, cax);
+  const double kscale = key_scale(A.cam, cax, valid ? px : 0, valid ? py : 0);
+  float Y[K];  // SH basis of this pixel's ray
+  sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
 
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
 
@@ -86,60 +94,86 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   double end_tau = kInf;
   uint32_t end_id = kNoPrim;
 
-  // Hit buffer: depth, alpha, tile-list position and Gaussian index of each
-  // pending hit, sorted by (depth, index); the (L,T) address is recomputed
-  // from the Gaussian's rectangle when the hit is composited, which keeps an
-  // entry at six registers.
-  double bt[KB], ba[KB];
-  uint32_t bc[KB], bid[KB];
-  int cnt = 0;
-  double e_tau = kInf;  // smallest dropped hit (all buffered hits are smaller)
-  uint32_t e_id = kNoPrim;
+  int head = 0, cnt = 0;  // ring: entries head, head + 1, ... (mod KB), sorted by (depth, index)
+  double e_tau = kInf;    // lower bound on the depths of dropped hits (every buffered hit is smaller)
+  float head_tf = __int_as_float(0x7f800000);  // depth bound of the ring's head (+inf if empty)
   uint32_t jr = UINT_MAX;  // first list position holding a dropped hit
   // A rescan starts the wave at the smallest jr of its lanes; a lane skips
   // the positions before its own jr (from): every hit there was composited
   // in an earlier pass.
   uint32_t from = 0;
-#pragma unroll
-  for (int s = 0; s < KB; ++s) {
-    bt[s] = kInf;
-    ba[s] = 0.0;
-    bc[s] = 0;
-    bid[s] = kNoPrim;
-  }
 
-  auto drop = [&](double t, uint32_t id, uint32_t c) {
+  // A dropped hit at list position c whose depth is at least t_lb.
+  auto drop = [&](double t_lb, uint32_t c) {
     ++n_drops;
-    if (key_less(t, id, e_tau, e_id)) {
-      e_tau = t;
-      e_id = id;
-    }
+    e_tau = fmin(e_tau, t_lb);
     jr = min(jr, c);
   };
 
+  // Exact depth of Gaussian id's max-response point on this lane's ray (the
+  // same evaluation as the trace's).
+  auto exact_tau = [&](uint32_t id) {
+    const double* G = A.geom + int64_t(kGeomStride) * id;
+    double W[9], og[3];
+#pragma unroll
+    for (int k = 0; k < 9; ++k) W[k] = G[kGeoW + k];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) og[k] = G[kGeoOg + k];
+    double tau, D2, xg[3];
+    ray_hit(W, og, G[kGeoD2c], d, &tau, &D2, xg);
+    return tau;
+  };
+
+  // Inserts a hit smaller than every dropped one into a ring with room:
+  // larger entries move up one slot, from the tail.
+  // (tau, id) < entry s of the ring in (depth, index) order, tu = tau
+  // rounded up to a float: rounding up is monotone, so unequal floats decide;
+  // a tie of the floats is decided on the entry's exact depth
+  auto before_entry = [&](double tau, float tu, uint32_t id, int s) {
+    const float st = s_btf[s][tid];
+    if (tu != st) return tu < st;
+    const uint32_t sid = s_bpid[s][tid].y;
+    return key_less(tau, id, exact_tau(sid), sid);
+  };
+
+  // Inserts a hit smaller than every dropped one into a ring with room:
+  // larger entries move up one slot, from the tail.
+  auto insert = [&](double tau, float tu, uint32_t id, uint32_t cpos, double a) {
+    int j = cnt;
+    while (j > 0) {
+      const int s = (head + j - 1) & (KB - 1);
+      if (!before_entry(tau, tu, id, s)) break;
+      const int t = (s + 1) & (KB - 1);
+      s_btf[t][tid] = s_btf[s][tid];
+      s_balpha[t][tid] = s_balpha[s][tid];
+      s_bpid[t][tid] = s_bpid[s][tid];
+      --j;
+    }
+    const int t = (head + j) & (KB - 1);
+    s_btf[t][tid] = tu;
+    s_balpha[t][tid] = a;
+    s_bpid[t][tid] = make_uint2(cpos, id);
+    if (j == 0) head_tf = tu;
+    ++cnt;
+  };
+
   auto composite_front = [&]() {
-    const double a = ba[0];
-    const uint32_t id = bid[0];
+    const double a = s_balpha[head][tid];
+    const uint2 pid = s_bpid[head][tid];
+    const uint32_t cpos = pid.x, id = pid.y;
     const float* shp = A.sh + int64_t(id) * (3 * K);
     const int4 rr = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
-    const int64_t lt_base = A.lt_offset[id] + lt_local_index(rr.x, rr.y, rr.z, rr.w, TILE, px, py);
+    const int64_t e = A.lt_offset[id] + lt_local_index(rr.x, rr.y, rr.z, rr.w, TILE, px, py);
     float c[3] = {0.5f, 0.5f, 0.5f};
 #pragma unroll
-    for (int k = 0; k < KP; k += 4) {
-      const float4 y4 = *reinterpret_cast<const float4*>(&s_Y[tid][k]);
-      const float yk[4] = {y4.x, y4.y, y4.z, y4.w};
+    for (int k = 0; k < K; ++k)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (k + u < K)
-#pragma unroll
-          for (int ch = 0; ch < 3; ++ch) c[ch] = fmaf(shp[3 * (k + u) + ch], yk[u], c[ch]);
-    }
+      for (int ch = 0; ch < 3; ++ch) c[ch] = fmaf(shp[3 * k + ch], Y[k], c[ch]);
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) c[ch] = fmaxf(c[ch], 0.0f);
     // k-th composited hit of this pixel -> its list position (read by the
     // gather backward)
-    A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = bc[0];
-    const int64_t e = lt_base;
+    A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = cpos;
     if constexpr (FMT == GART_LT_FULL) {
       A.lt[e] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
                            color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
@@ -164,26 +198,88 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
     L2 = fma(w, double(c[2]), L2);
     T = T * (1.0 - a);
     ++n_hits;
-    last_tau = bt[0];
     last_id = id;
-    if (T < A.t_min) {
+    if (T < A.t_min) {  // terminated; its exact depth is found after the trace
       done = true;
-      end_tau = bt[0];
       end_id = id;
     }
-#pragma unroll
-    for (int s = 0; s + 1 < KB; ++s) {
-      bt[s] = bt[s + 1];
-      ba[s] = ba[s + 1];
-      bc[s] = bc[s + 1];
-      bid[s] = bid[s + 1];
-    }
-    bt[KB - 1] = kInf;  // unused slots hold depth +inf
+    head = (head + 1) & (KB - 1);
     --cnt;
+    head_tf = cnt > 0 ? s_btf[head][tid] : __int_as_float(0x7f800000);
   };
 
   uint32_t restart = 0;
-  int passes = 0;
+  int passes = 0;  // rescans so far
+
+  // One staged candidate: geometry row, rectangle and index.
+  struct Cand {
+    double W[9], og[3], D2c, sig;
+    int4 r;
+    uint32_t id;
+  };
+  auto load_cand = [&](int c) {
+    const double* row = s_row + c * kRow;
+    Cand cd;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) cd.W[k] = row[k];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) cd.og[k] = row[9 + k];
+    cd.D2c = row[12];
+    cd.sig = row[13];
+    cd.r = *reinterpret_cast<const int4*>(row + 16);
+    cd.id = reinterpret_cast<const uint32_t*>(row + 18)[0];
+    return cd;
+  };
+
+  // Tests candidate c of the batch starting at list position base against
+  // this lane's ray, buffers a hit, and at the flush points composites the
+  // hits that are final.  Returns true when the lane leaves the batch
+  // (terminated, or stalled until a rescan).
+  auto visit = [&](const Cand& cd, int c, int nb, int64_t base) -> bool {
+    const uint32_t cpos = uint32_t(base - beg) + uint32_t(c);
+    const bool inside = (cpos >= from) & (px >= cd.r.x) & (px <= cd.r.z) & (py >= cd.r.y) & (py <= cd.r.w);
+    if (inside) {
+      ++n_tests;
+      double tau, D2, xg[3];
+      const uint32_t id = cd.id;
+      // in a rescan, hits up to the last composited one were composited before
+      if (ray_hit(cd.W, cd.og, cd.D2c, d, &tau, &D2, xg) && (passes == 0 || key_less(last_tau, last_id, tau, id))) {
+        if (!(tau < e_tau)) {
+          drop(tau, cpos);
+        } else {
+          const float tu = __double2float_ru(tau);
+          bool ins = true;
+          if (cnt == KB) {  // full: the larger of the new hit and the tail is dropped
+            const int s = (head + KB - 1) & (KB - 1);
+            if (!before_entry(tau, tu, id, s)) {
+              drop(tau, cpos);
+              ins = false;
+            } else {
+              // the tail's depth is above the float below its rounded-up bound
+              const float tf = s_btf[s][tid];  // > 0 (a hit has tau > 0)
+              drop(double(__uint_as_float(__float_as_uint(tf) - 1u)), s_bpid[s][tid].x);
+              cnt = KB - 1;
+            }
+          }
+          if (ins) insert(tau, tu, id, cpos, cd.sig * exp(-0.5 * D2));
+        }
+      }
+    }
+    // Composite the final hits every kFlushEvery Gaussians, at the end of a
+    // batch, and whenever a lane's ring is full -- for every lane of the wave
+    // at once, so that each compositing step serves more lanes.
+    if (__ballot((c + 1) % kFlushEvery == 0 || c + 1 == nb || cnt == KB) != 0) {
+      const double nk = double(s_key[c + 1]) * kscale;
+      while (cnt > 0 && !done && double(head_tf) < nk) composite_front();
+      if (done) return true;
+      if (e_tau < kInf && nk > e_tau) {
+        stalled = true;
+        return true;
+      }
+    }
+    return false;
+  };
+
   for (;;) {
     for (int64_t base = beg + restart; base < end; base += NB) {
       const int nb = int(min<int64_t>(NB, end - base));
@@ -213,92 +309,15 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
           // The candidate's whole staged row is read at once (one LDS round
           // trip; every lane reads the same address), then the rectangle
           // decides which lanes test it.
-          const double* row = s_row + c * kRow;
-          const int4 r = *reinterpret_cast<const int4*>(row + 16);
-          double W[9], og[3];
-#pragma unroll
-          for (int k = 0; k < 9; ++k) W[k] = row[k];
-#pragma unroll
-          for (int k = 0; k < 3; ++k) og[k] = row[9 + k];
-          double D2c = row[12], sig = row[13];
-          uint32_t id = reinterpret_cast<const uint32_t*>(row + 18)[0];
+          Cand cd = load_cand(c);
           // materialise the row here, so that the compiler does not sink its
           // reads into the branch (a second LDS round trip per candidate)
 #pragma unroll
-          for (int k = 0; k < 9; ++k) asm volatile("" : "+v"(W[k]));
+          for (int k = 0; k < 9; ++k) asm volatile("" : "+v"(cd.W[k]));
 #pragma unroll
-          for (int k = 0; k < 3; ++k) asm volatile("" : "+v"(og[k]));
-          asm volatile("" : "+v"(D2c), "+v"(sig), "+v"(id));
-          const bool inside = (uint32_t(base - beg) + uint32_t(c) >= from) & (px >= r.x) & (px <= r.z) &
-                              (py >= r.y) & (py <= r.w);
-          if (inside) {
-            ++n_tests;
-            double tau, D2, xg[3];
-            if (ray_hit(W, og, D2c, d, &tau, &D2, xg) && key_less(last_tau, last_id, tau, id)) {
-              const uint32_t cpos = uint32_t(base - beg) + uint32_t(c);
-              if (!key_less(tau, id, e_tau, e_id)) {
-                drop(tau, id, cpos);
-              } else {
-                bool ins = true;
-                if (cnt == KB) {
-                  if (!key_less(tau, id, bt[KB - 1], bid[KB - 1])) {
-                    drop(tau, id, cpos);
-                    ins = false;
-                  } else {
-                    drop(bt[KB - 1], bid[KB - 1], bc[KB - 1]);
-                    cnt = KB - 1;
-                  }
-                }
-                if (ins) {
-                  const double a = sig * exp(-0.5 * D2);
-                  // Position = entries with a smaller (depth, index) key.
-                  // Unused slots hold depth +inf, so a strict depth count
-                  // needs no occupancy test; equal depths (rare) also count
-                  // the entries of smaller index.  Shift and placement are
-                  // selects, not branches.
-                  int pos = 0;
-                  bool tie = false;
-#pragma unroll
-                  for (int s = 0; s < KB; ++s) {
-                    pos += bt[s] < tau ? 1 : 0;
-                    tie = tie || bt[s] == tau;
-                  }
-                  if (tie) {
-#pragma unroll
-                    for (int s = 0; s < KB; ++s) pos += (bt[s] == tau && bid[s] < id) ? 1 : 0;
-                  }
-#pragma unroll
-                  for (int s = KB - 1; s >= 1; --s) {
-                    const bool sh = s > pos, pl = s == pos;
-                    bt[s] = sh ? bt[s - 1] : (pl ? tau : bt[s]);
-                    ba[s] = sh ? ba[s - 1] : (pl ? a : ba[s]);
-                    bc[s] = sh ? bc[s - 1] : (pl ? cpos : bc[s]);
-                    bid[s] = sh ? bid[s - 1] : (pl ? id : bid[s]);
-                  }
-                  if (pos == 0) {
-                    bt[0] = tau;
-                    ba[0] = a;
-                    bc[0] = cpos;
-                    bid[0] = id;
-                  }
-                  ++cnt;
-                }
-              }
-            }
-          }
-          // Composite the final hits every kFlushEvery Gaussians, at the end
-          // of a batch, and whenever a lane's buffer is full -- for every
-          // lane of the wave at once, so that each compositing step serves
-          // more lanes.
-          if (__ballot((c + 1) % kFlushEvery == 0 || c + 1 == nb || cnt == KB) != 0) {
-            const double nk = double(s_key[c + 1]);
-            while (cnt > 0 && bt[0] < nk && !done) composite_front();
-            if (done) break;
-            if (e_tau < kInf && nk > e_tau) {
-              stalled = true;
-              break;
-            }
-          }
+          for (int k = 0; k < 3; ++k) asm volatile("" : "+v"(cd.og[k]));
+          asm volatile("" : "+v"(cd.D2c), "+v"(cd.sig), "+v"(cd.id));
+          if (visit(cd, c, nb, base)) break;
         }
       }
       const bool busy = !done && !finished && !stalled;
@@ -325,13 +344,16 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
     if (need) {
       from = jr;
       e_tau = kInf;
-      e_id = kNoPrim;
       jr = UINT_MAX;
       stalled = false;
       cnt = 0;
+      head = 0;
+      head_tf = __int_as_float(0x7f800000);
+      last_tau = n_hits ? exact_tau(last_id) : -kInf;  // for the skip test of the rescan
     }
   }
 
+  if (end_id != kNoPrim) end_tau = exact_tau(end_id);
   if (valid) {
     const int64_t p = int64_t(py) * A.cam.W + px;
     A.image[3 * p + 0] = float(L0);
@@ -356,21 +378,39 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   }
 }
 
-template <int TILE, int K>
-hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
+// Ring sizes: deep frames (long tile lists, many pending hits per ray) get
+// the larger ring; it costs occupancy (LDS), so others get the smaller.
+#ifndef GART_FWD_RING_SMALL
+#define GART_FWD_RING_SMALL 8
+#endif
+#ifndef GART_FWD_RING_LARGE
+#define GART_FWD_RING_LARGE 16
+#endif
+constexpr int64_t kDeepListPairs = 2048;  // mean pairs per tile from which a frame counts as deep
+
+template <int TILE, int K, int KB>
+hipError_t launch_ring(const ForwardArgs& a, hipStream_t s) {
   const int n_tiles = a.tiles_x * a.tiles_y;
-  hipError_t e = record(a.ev_begin, s);
-  if (e != hipSuccess) return e;
   switch (a.lt_format) {
-    case GART_LT_FULL: forward_kernel<TILE, K, GART_LT_FULL><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
-    case GART_LT_T_ONLY: forward_kernel<TILE, K, GART_LT_T_ONLY><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
-    case GART_LT_HALF: forward_kernel<TILE, K, GART_LT_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
-    case GART_LT_T_HALF: forward_kernel<TILE, K, GART_LT_T_HALF><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
-    case GART_LT_FIXED16: forward_kernel<TILE, K, GART_LT_FIXED16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
-    case GART_LT_T_LOG16: forward_kernel<TILE, K, GART_LT_T_LOG16><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_FULL: forward_kernel<TILE, K, GART_LT_FULL, KB><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_T_ONLY: forward_kernel<TILE, K, GART_LT_T_ONLY, KB><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_HALF: forward_kernel<TILE, K, GART_LT_HALF, KB><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_T_HALF: forward_kernel<TILE, K, GART_LT_T_HALF, KB><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_FIXED16: forward_kernel<TILE, K, GART_LT_FIXED16, KB><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
+    case GART_LT_T_LOG16: forward_kernel<TILE, K, GART_LT_T_LOG16, KB><<<n_tiles, TILE * TILE, 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+template <int TILE, int K>
+hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
+  hipError_t e = record(a.ev_begin, s);
+  if (e != hipSuccess) return e;
+  const int64_t n_tiles = int64_t(a.tiles_x) * a.tiles_y;
+  const bool deep = a.pair_count > kDeepListPairs * n_tiles;
+  e = deep ? launch_ring<TILE, K, GART_FWD_RING_LARGE>(a, s) : launch_ring<TILE, K, GART_FWD_RING_SMALL>(a, s);
+  if (e != hipSuccess) return e;
   return record(a.ev_end, s);
 }
 

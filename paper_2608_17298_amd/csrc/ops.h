@@ -77,7 +77,7 @@ struct TileMapArgs {
   int64_t* pair_offset;     // [n+1] first pair slot of each Gaussian (tile counts, scanned in place)
   uint32_t* keys;           // [P] (tile << key_bits) | depth code of each emitted pair
   uint32_t* vals;           // [P] emitted Gaussian indices
-  float* pair_key;          // [P] depth bound of each sorted pair (decoded code)
+  float* pair_key;          // [P] camera-depth bound of each sorted pair (decoded code)
   int32_t key_bits;         // bits of the depth code in keys
   int64_t pair_count;
   int64_t* tile_range;      // [n_tiles+1]
@@ -95,7 +95,7 @@ struct ForwardArgs {
   double t_min;
   const int64_t* tile_range;
   const uint32_t* pair_prim;
-  const float* pair_key;     // [pairs] depth lower bound of each pair (ascending in a tile list)
+  const float* pair_key;     // [pairs] camera-depth lower bound of each pair (ascending in a tile list)
   const double* geom;
   const int32_t* rect;
   const int64_t* lt_offset;
@@ -107,6 +107,7 @@ struct ForwardArgs {
   gart_pixel_state* pixel_state;
   uint32_t* hit_list;       // [pairs * tile^2] list position of each pixel's k-th composited hit
   uint32_t* status;         // frame status word (GART_FRAME_* bits), cleared before the launch
+  int64_t pair_count;       // pairs in the tile lists (sizes the per-lane pending-hit rings)
   uint64_t* counters;
   void* ev_begin;  // optional hipEvent_t recorded around the kernel
   void* ev_end;
@@ -120,7 +121,7 @@ struct BackwardArgs {
   int64_t n;
   const int64_t* tile_range;
   const uint32_t* pair_prim;
-  const float* pair_key;     // [pairs] depth lower bound of each pair (ascending in a tile list)
+  const float* pair_key;     // [pairs] camera-depth lower bound of each pair (ascending in a tile list)
   const double* geom;
   const int32_t* rect;
   const int64_t* lt_offset;

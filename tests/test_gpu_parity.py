@@ -149,16 +149,20 @@ def test_tile_lists_bit_exact(name):
 @pytest.mark.parametrize("name", ["small_reduced", "1m_reduced", "stress_reduced", "random_sh3_tile16",
                                   "rotated_sh3"])
 def test_pair_keys_bound_every_hit(name):
-    """Each pair's key is at most the oracle's tau (Eq. 3) at every pixel of
-    its tile where the ray hits the Gaussian: the forward's early compositing
-    and the backward's list cut-off rely on it."""
+    """Each pair's key is at most tau_q / s_q at every pixel q of its tile
+    where the ray hits the Gaussian (gart_frame.pair_key): tau_q from the
+    oracle's max-response point (Eq. 3-5), s_q = |R^T u_q| / (c . u_q) for
+    the pixel's camera ray u_q = (a, b, 1) and c the unit camera-space
+    direction through the tile centre.  The forward's early compositing and
+    the backward's list cut-off rely on it."""
     sc, o, info, ren, grads, gpu = _case(name)
     ts, W = sc.tile, o.W
+    cam = sc.camera
     tx_n = (W + ts - 1) // ts
     rng = np.random.default_rng(7)
     P = gpu["pair_count"]
     sel = rng.choice(P, min(P, 4000), replace=False)
-    pix, prims, keys = [], [], []
+    pix, prims, keys, axes = [], [], [], []
     for j in sel:
         t, i = int(gpu["pair_tile"][j]), int(gpu["pair_prim"][j])
         x0, y0, x1, y1 = info.rect[i]
@@ -170,11 +174,16 @@ def test_pair_keys_bound_every_hit(name):
         pix.append(p)
         prims.append(np.full(p.size, i))
         keys.append(np.full(p.size, gpu["pair_key"][j], np.float64))
-    pix, prims, keys = np.concatenate(pix), np.concatenate(prims), np.concatenate(keys)
+        c = np.array([((tx + 0.5) * ts - cam.cx) / cam.fx, ((ty + 0.5) * ts - cam.cy) / cam.fy, 1.0])
+        axes.append(np.tile(c / np.linalg.norm(c), (p.size, 1)))
+    pix, prims, keys, axes = np.concatenate(pix), np.concatenate(prims), np.concatenate(keys), np.concatenate(axes)
     r = o.ray_prim(pix, prims)
     hit = r["hit"]
     assert hit.any()
-    assert np.all(keys[hit] <= r["tau"][hit]), np.max(keys[hit] - r["tau"][hit])
+    u = np.stack([(pix % W + 0.5 - cam.cx) / cam.fx, (pix // W + 0.5 - cam.cy) / cam.fy, np.ones(pix.size)], 1)
+    s_q = np.linalg.norm(u @ np.asarray(cam.R, np.float64), axis=1) / np.einsum("ij,ij->i", u, axes)
+    depth = r["tau"] / s_q
+    assert np.all(keys[hit] <= depth[hit]), np.max(keys[hit] - depth[hit])
     # the per-tile bound is not vacuous: most hit pairs get a positive key
     assert np.mean(keys[hit] > 0) > 0.5
 
