@@ -37,6 +37,28 @@ STATE_CULLED_BEHIND = 2
 STATE_CULLED_OFFSCREEN = 3
 STATE_CULLED_NONFINITE = 4
 
+# Storage of (L, T) in the intermediate buffer, as the backward reads it back:
+#   exact    L and T as composited
+#   half     L and T rounded to float, then to the nearest fp16
+#   t_half   T only (the colour behind a hit summed back to front from the
+#            later hits with their stored T), T as in ``half``
+#   fixed16  L in units of B / 2^16 (B = ``OracleScene.colour_bound``),
+#            T = 2^(-q / 4096) with q = round(-log2(T) 4096)
+#   t_log16  T only, coded as in ``fixed16``, colour behind as in ``t_half``
+#   t_float  T only, rounded to float, colour behind as in ``t_half``
+STORAGE_MODELS = {"exact": 0, "half": 1, "t_half": 2, "fixed16": 3, "t_log16": 4, "t_float": 5}
+
+
+def storage_round(kind: str, x, unit: float = 1.0):
+    """The rounding of a stored value: ``half`` (float, then fp16, ties to
+    even), ``fixed16`` (L in units of ``unit``, saturating at 65535 units)
+    or ``log16`` (the transmittance code of ``fixed16``)."""
+    x = _c(x, np.float64).ravel()
+    out = np.zeros_like(x)
+    lib().orc_storage_round({"half": 1, "fixed16": 2, "log16": 3}[kind], x.shape[0], _ptr(x), _ptr(out),
+                            float(unit))
+    return out
+
 
 def build(force: bool = True) -> str:
     """Compile the oracle with g++ (fp64, OpenMP, no fast-math)."""
@@ -75,6 +97,10 @@ def lib():
         L.orc_all_hits.argtypes = [P, i64, P, i32, i32, P, P, P]
         L.orc_records.argtypes = [P, i64, P, P, P, P, P]
         L.orc_backward.argtypes = [P, i64, P, P, P, P, P, P, P]
+        L.orc_backward_stored.argtypes = [P, i64, P, P, P, P, P, P, P, i32]
+        L.orc_storage_round.argtypes = [i32, i64, P, P, ctypes.c_double]
+        L.orc_colour_bound.restype = ctypes.c_double
+        L.orc_colour_bound.argtypes = [P]
         L.orc_lt_index.argtypes = [P, i32, i64, P, P, P]
         L.orc_num_threads.restype = i32
         _lib = L
@@ -232,8 +258,12 @@ class OracleScene:
         lib().orc_records(self.h, m, _ptr(pix), _ptr(off), _ptr(prim), _ptr(LT), _ptr(tau))
         return off, prim, LT, tau
 
-    def backward(self, dl_dimage, pixels=None):
-        """Raw-parameter gradients of sum <dL/dC, C> over the listed pixels (all if None)."""
+    def backward(self, dl_dimage, pixels=None, storage="exact"):
+        """Raw-parameter gradients of sum <dL/dC, C> over the listed pixels (all if None).
+
+        ``storage`` names how the intermediate buffer keeps (L, T) (Sec. 6
+        suggests fp16): the gradient is the plain one with L and T replaced
+        by their stored values (``STORAGE_MODELS``)."""
         dl = _c(dl_dimage, np.float64).reshape(self.H, self.W, 3)
         if pixels is None:
             m, pix = 0, None
@@ -243,9 +273,14 @@ class OracleScene:
         n, K = self.n, self.K
         g = dict(means=np.zeros((n, 3)), log_scales=np.zeros((n, 3)), quats=np.zeros((n, 4)),
                  logits=np.zeros(n), sh=np.zeros((n, K, 3)))
-        lib().orc_backward(self.h, m, _ptr(pix), _ptr(dl), _ptr(g["means"]), _ptr(g["log_scales"]),
-                           _ptr(g["quats"]), _ptr(g["logits"]), _ptr(g["sh"]))
+        lib().orc_backward_stored(self.h, m, _ptr(pix), _ptr(dl), _ptr(g["means"]), _ptr(g["log_scales"]),
+                                  _ptr(g["quats"]), _ptr(g["logits"]), _ptr(g["sh"]), STORAGE_MODELS[storage])
         return g
+
+    def colour_bound(self) -> float:
+        """B of the ``fixed16`` storage model: the largest colour any visible
+        Gaussian can give in any direction, raised by 2^-16."""
+        return float(lib().orc_colour_bound(self.h))
 
     def lt_index(self, tile: int, prims, pixels):
         """idx(i,t,p) of Eq. 16 by enumeration; -1 outside the rectangle."""

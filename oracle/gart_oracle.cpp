@@ -618,6 +618,70 @@ void orc_records(void* h, int64_t npix, const int64_t* pix, const int64_t* offse
   }
 }
 
+// Reduced-precision storage of the intermediate buffer (Sec. 6 suggests
+// fp16).  The backward reads L and T back from the buffer, so the gradient a
+// storage format yields is the plain gradient with L and T replaced by their
+// stored values.  Models (each a reading of what the format keeps):
+//   0  exact L and T (float T, fixed-point L are exact to ~1e-7)
+//   1  L and T each rounded to float, then to the nearest fp16
+//   2  T only (hybrid backward), rounded to float then fp16; the colour behind
+//      a hit is summed from the later hits with their stored T
+//   3  L in 16-bit fixed point with unit B / 2^16 (B = the frame's colour
+//      bound), T as the code q = round(-log2(T) 4096), T = 2^(-q / 4096)
+//   4  T only (hybrid backward) as the code of model 3, colour behind summed
+//      as in model 2
+//   5  T only (hybrid backward), T rounded to float, colour behind summed as
+//      in model 2
+// Rounds x (a float) to the nearest fp16, ties to even (normal and
+// subnormal fp16 range; the values stored here are far below its maximum).
+double round_half(double x) {
+  const double f = double(float(x));
+  const double a = std::fabs(f);
+  if (a == 0.0) return f;
+  double q;  // fp16 spacing at a
+  if (a < std::ldexp(1.0, -14)) {
+    q = std::ldexp(1.0, -24);
+  } else {
+    int e;
+    std::frexp(a, &e);           // a = m 2^e, m in [0.5, 1)
+    q = std::ldexp(1.0, e - 11);  // 11 significant bits
+  }
+  return std::nearbyint(f / q) * q;  // the default rounding mode is to nearest, ties to even
+}
+
+// L in model 3's fixed point with unit q (saturating at 65535 units).
+double round_fixed16(double L, double q) { return std::min(std::nearbyint(L / q), 65535.0) * q; }
+
+// T through the 16-bit logarithmic code of model 3.
+double round_log16(double T) {
+  const double q = std::min(std::nearbyint(-std::log2(double(float(T))) * 4096.0), 65535.0);
+  return std::exp2(-q / 4096.0);
+}
+
+// The frame's colour bound B (model 3): over every visible Gaussian and
+// channel, 1/2 + sum_l sqrt((2l + 1) / (4 pi)) |sh_l| (the largest |colour|
+// any direction can give, by Cauchy-Schwarz and the SH addition theorem),
+// raised by 2^-16.
+double colour_bound(const Scene& S) {
+  double B = 0.0;
+  for (int64_t i = 0; i < S.n; ++i) {
+    if (S.prims[i].state != kActive) continue;
+    for (int ch = 0; ch < 3; ++ch) {
+      double v = 0.5;
+      for (int l = 0; l <= S.deg; ++l) {
+        double ss = 0.0;
+        for (int m = -l; m <= l; ++m) {
+          const double k = S.sh[(i * S.K + l * l + l + m) * 3 + ch];
+          ss += k * k;
+        }
+        v += std::sqrt(ss * (2.0 * l + 1.0) / (4.0 * kPi));
+      }
+      B = std::max(B, v);
+    }
+  }
+  return (B > 0.0 ? B : 1.0) * (1.0 + std::ldexp(1.0, -16));
+}
+
 // Gradient of L = sum_p <dL/dC_p, C_p> over the listed pixels (null = all),
 // with respect to the raw parameters: means, log-scales, the unnormalised
 // quaternion, opacity logits and SH coefficients.  Outputs are overwritten.
@@ -633,9 +697,10 @@ void orc_records(void* h, int64_t npix, const int64_t* pix, const int64_t* offse
 //   dL/dW  += dL/do_g (o - mu)^T + dL/dd_g d^T,   dL/dmu += -W^T dL/do_g.
 // Per primitive: W = S^-1 R^T gives dL/dlog s_k = -sum_j dW_kj W_kj and
 // dL/dR_jk = dW_kj / s_k; the quaternion gradient goes through R(q/|q|).
-void orc_backward(void* h, int64_t npix, const int64_t* pix, const double* dl_dimage, double* g_means,
-                  double* g_log_scales, double* g_quats, double* g_logits, double* g_sh) {
+void orc_backward_stored(void* h, int64_t npix, const int64_t* pix, const double* dl_dimage, double* g_means,
+                         double* g_log_scales, double* g_quats, double* g_logits, double* g_sh, int32_t model) {
   Scene& S = *static_cast<Scene*>(h);
+  const double lq = model == 3 ? colour_bound(S) * std::ldexp(1.0, -16) : 1.0;  // model 3 unit of L
   const int64_t n = S.n;
   const int K = S.K;
   std::vector<double> accW(n * 9, 0.0), accMu(n * 3, 0.0), accSig(n, 0.0), accSh(n * K * 3, 0.0);
@@ -656,16 +721,39 @@ void orc_backward(void* h, int64_t npix, const int64_t* pix, const double* dl_di
       pixel_ray(S, px, py, d);
       sh_basis(S.deg, d, Y.data());
       double g[3] = {dl_dimage[3 * p], dl_dimage[3 * p + 1], dl_dimage[3 * p + 2]};
-      for (const Composited& c : comp) {
+      // stored T of each hit and, for the T-only models, the colour behind
+      // each hit summed from the later hits (back to front)
+      const size_t nc = comp.size();
+      std::vector<double> Ts(nc), walk(3 * (nc + 1), 0.0);
+      for (size_t k = 0; k < nc; ++k) {
+        const double T = comp[k].T;
+        Ts[k] = (model == 1 || model == 2) ? round_half(T)
+                : (model == 3 || model == 4) ? round_log16(T)
+                : model == 5                 ? double(float(T))
+                                             : T;
+      }
+      for (size_t k = nc; k-- > 0;)
+        for (int ch = 0; ch < 3; ++ch)
+          walk[3 * k + ch] = walk[3 * (k + 1) + ch] + Ts[k] * comp[k].alpha * comp[k].c[ch];
+      for (size_t k = 0; k < nc; ++k) {
+        const Composited& c = comp[k];
         const Prim& P = S.prims[c.id];
+        const double Tst = Ts[k];
         double behind[3], dLdalpha = 0.0;
         for (int ch = 0; ch < 3; ++ch) {
-          behind[ch] = r.C[ch] - c.L[ch] - c.T * c.alpha * c.c[ch];
-          dLdalpha += g[ch] * (c.T * c.c[ch] - behind[ch] / (1.0 - c.alpha));
+          if (model == 2 || model == 4 || model == 5) {
+            behind[ch] = walk[3 * (k + 1) + ch];
+          } else {
+            double L = c.L[ch];
+            if (model == 1) L = round_half(L);
+            if (model == 3) L = round_fixed16(L, lq);
+            behind[ch] = r.C[ch] - L - Tst * c.alpha * c.c[ch];
+          }
+          dLdalpha += g[ch] * (Tst * c.c[ch] - behind[ch] / (1.0 - c.alpha));
         }
         for (int ch = 0; ch < 3; ++ch) {
           if (!c.unclamped[ch]) continue;
-          double dc = c.T * c.alpha * g[ch];
+          double dc = Tst * c.alpha * g[ch];
           for (int k = 0; k < K; ++k) atomic_add(&accSh[(c.id * K + k) * 3 + ch], dc * Y[k]);
         }
         double rho = std::exp(-0.5 * c.D2);
@@ -725,6 +813,21 @@ void orc_backward(void* h, int64_t npix, const int64_t* pix, const double* dl_di
     for (int k = 0; k < K * 3; ++k) g_sh[i * K * 3 + k] = accSh[i * K * 3 + k];
   }
 }
+
+void orc_backward(void* h, int64_t npix, const int64_t* pix, const double* dl_dimage, double* g_means,
+                  double* g_log_scales, double* g_quats, double* g_logits, double* g_sh) {
+  orc_backward_stored(h, npix, pix, dl_dimage, g_means, g_log_scales, g_quats, g_logits, g_sh, 0);
+}
+
+// A stored value's rounding applied to m values (for the pins): kind 1 the
+// fp16 of model 1, 2 model 3's L with unit q, 3 model 3's T.
+void orc_storage_round(int32_t kind, int64_t m, const double* x, double* out, double q) {
+  for (int64_t k = 0; k < m; ++k)
+    out[k] = kind == 1 ? round_half(x[k]) : kind == 2 ? round_fixed16(x[k], q) : round_log16(x[k]);
+}
+
+// The colour bound B of model 3.
+double orc_colour_bound(void* h) { return colour_bound(*static_cast<Scene*>(h)); }
 
 // Intermediate-buffer address idx(i, t, p) = O_prim(i) + O_tile(i, t) +
 // O_pixel(i, t, p) (Eq. 16, Sec. 4.3), by plain counting:
