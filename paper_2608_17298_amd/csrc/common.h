@@ -273,8 +273,9 @@ __device__ __forceinline__ float lt_T(uint4 v) {
 // C - L of channel ch (final colour minus the colour in front of the hit),
 // from the pixel's fixed-point C and a loaded FULL, HALF or FIXED16 entry.
 // FULL and FIXED16: an exact integer difference in units of step (the 16-bit
-// L is in units of step * 2^16), then one rounding; HALF: C (float) minus the
-// fp16 L.
+// L is in units of step * 2^16), then one rounding; HALF: C minus the fp16 L
+// in fp64 (one fused rounding of the exact C and L), then to float, so that
+// deep hits, where L is close to C, keep the stored L's precision.
 template <int FMT>
 __device__ __forceinline__ float lt_c_minus_l(uint4 v, const uint32_t Cq[3], int ch, float step) {
   if constexpr (FMT == GART_LT_FULL) {
@@ -285,7 +286,7 @@ __device__ __forceinline__ float lt_c_minus_l(uint4 v, const uint32_t Cq[3], int
     if constexpr (FMT == GART_LT_FIXED16)
       return float(int64_t(Cq[ch]) - int64_t(hb & 0xffffu) * 65536) * step;
     else
-      return __uint2float_rn(Cq[ch]) * step - half_value(hb);
+      return float(fma(double(Cq[ch]), double(step), -double(half_value(hb))));
   }
 }
 

@@ -409,7 +409,9 @@ hipError_t launch_t(const ForwardArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   const int64_t n_tiles = int64_t(a.tiles_x) * a.tiles_y;
   const bool deep = a.pair_count > kDeepListPairs * n_tiles;
-  e = deep ? launch_ring<TILE, K, GART_FWD_RING_LARGE>(a, s) : launch_ring<TILE, K, GART_FWD_RING_SMALL>(a, s);
+  // 16x16 tiles hold four waves' rings per workgroup: at most 16 entries each
+  constexpr int kLarge = TILE == 8 ? GART_FWD_RING_LARGE : (GART_FWD_RING_LARGE < 16 ? GART_FWD_RING_LARGE : 16);
+  e = deep ? launch_ring<TILE, K, kLarge>(a, s) : launch_ring<TILE, K, GART_FWD_RING_SMALL>(a, s);
   if (e != hipSuccess) return e;
   return record(a.ev_end, s);
 }

@@ -131,3 +131,16 @@ def per_gaussian_err(a, b, floor_frac=1e-3):
     if rms == 0.0:
         return float(np.abs(a).max())
     return float((np.linalg.norm(a - b, axis=1) / np.maximum(nb, floor_frac * rms)).max())
+
+
+def max_abs_over_rms(a, b):
+    """Largest per-Gaussian difference of one gradient group, |a_i - b_i|,
+    over the RMS of the reference rows."""
+    a = np.asarray(a, np.float64).reshape(len(a), -1)
+    b = np.asarray(b, np.float64).reshape(len(b), -1)
+    if b.size == 0:
+        return 0.0
+    nb = np.linalg.norm(b, axis=1)
+    rms = np.sqrt(np.mean(nb * nb))
+    d = np.linalg.norm(a - b, axis=1)
+    return float(d.max() / rms) if rms > 0 else float(d.max())

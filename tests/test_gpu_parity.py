@@ -9,8 +9,8 @@ import numpy as np
 import pytest
 
 import oracle
-from helpers import (dc_for_colour, l1_upstream, per_gaussian_err, random_tiny_scene, rel_l2, rotated_camera,
-                     run_gpu, small_camera)
+from helpers import (dc_for_colour, l1_upstream, max_abs_over_rms, per_gaussian_err, random_tiny_scene, rel_l2,
+                     rotated_camera, run_gpu, small_camera)
 from paper_2608_17298_amd.scenes import custom_scene, make_scene
 
 pytestmark = pytest.mark.gpu
@@ -309,30 +309,51 @@ def test_gather_wave_units(name):
     assert gart.CNT_BWD_WAVE_UNITS == 10
 
 
-# Reduced-precision intermediate storage (Sec. 6 suggests fp16).  Bars:
-# 2x the largest relative-L2 error measured over these scenes.  fp16 (the
-# paper's suggestion) misses the 1e-4 gradient bar by about 10x; 16-bit
-# fixed-point L with a 16-bit log-coded T misses it by about 1.4x; the
-# hybrid mode's 2-byte log-coded T meets it.
-STORAGE_BARS = {("gather", "half"): 2.1e-3, ("hybrid", "half"): 6e-4, ("scatter", "half"): 2.1e-3,
-                ("gather", "fixed16"): 2.9e-4, ("hybrid", "fixed16"): 1e-4, ("scatter", "fixed16"): 2.9e-4}
+# Reduced-precision intermediate storage (Sec. 6 suggests fp16).  Each
+# layout is checked against the oracle's model of it: the backward with L and
+# T replaced by their stored values (the T-only layouts of the hybrid mode
+# sum the colour behind a hit from the stored T of the later hits).
+#
+# The two sides' L and T differ by fp32 colour rounding (~1e-7 relative), so
+# a stored value within that distance of a rounding boundary may land on the
+# neighbouring code on one side only: a fraction p ~ 2e-7 |L| / q of the
+# values (q the quantum: fp16 2^-11 |L|, fixed16 B / 2^16; p < 0.5% here).
+# Such a value errs by a whole quantum where the model's own rounding errs by
+# q / sqrt(12) on average, so the residual is about sqrt(12 p) < 0.25 of the
+# storage effect itself, rel_l2(model, exact); in a small scene a single
+# heavy hit can carry it, so the bar is 0.3 of the storage effect, and never
+# below the full-precision 1e-4.  Per Gaussian the check is absolute: one
+# quantum divided by 1 - alpha can be all of a small gradient, so the bar is
+# |g_i - m_i| <= 1e-2 x the group's RMS (2^-11, one fp16 quantum of a unit
+# colour, times the 1 / (1 - alpha) of alpha = 0.95).
+STORAGE_MODEL = {("gather", "half"): "half", ("scatter", "half"): "half", ("hybrid", "half"): "t_half",
+                 ("gather", "fixed16"): "fixed16", ("scatter", "fixed16"): "fixed16",
+                 ("hybrid", "fixed16"): "t_log16"}
+STORAGE_FLIP_FRAC = 0.3
+STORAGE_ELEM_TOL = 1e-2
 
 
-# The bars hold for the workload-like scenes.  The nearly opaque scene is left
-# out: a quantised L enters the colour behind a hit divided by 1 - alpha,
-# which reaches ~1e-8 there, so no storage-only bar applies to it.
-STORAGE_SCENES = [s for s in SCENES if s != "opaque_sh3"]
+def _storage_grads(name, model):
+    key = ("oracle_storage", name, model)
+    if key not in _cache:
+        sc = _cache[("scene", name)]
+        _cache[key] = _cache[("oracle", name)][0].backward(sc.dl_dimage, storage=model)
+    return _cache[key]
 
 
-@pytest.mark.parametrize("mode,prec", sorted(STORAGE_BARS))
-@pytest.mark.parametrize("name", STORAGE_SCENES)
+@pytest.mark.parametrize("mode,prec", sorted(STORAGE_MODEL))
+@pytest.mark.parametrize("name", SCENES)
 def test_backward_reduced_storage(name, mode, prec):
     sc, o, info, ren, grads, ref = _case(name, mode)
     gpu = run_gpu(sc, mode=mode, precision=prec)
     assert np.array_equal(gpu["image"], ref["image"])  # storage does not change the forward's result
+    model = _storage_grads(name, STORAGE_MODEL[(mode, prec)])
     for k in GROUPS:
-        e = rel_l2(gpu["grads"][k], grads[k])
-        assert e <= STORAGE_BARS[(mode, prec)], (k, e)
+        e = rel_l2(gpu["grads"][k], model[k])
+        assert e <= max(GRAD_TOL, STORAGE_FLIP_FRAC * rel_l2(model[k], grads[k])), (k, e)
+        assert np.isfinite(gpu["grads"][k]).all(), k
+        pe = max_abs_over_rms(gpu["grads"][k], model[k])
+        assert pe <= STORAGE_ELEM_TOL, (k, pe)
 
 
 @pytest.mark.parametrize("prec", ["half", "fixed16"])
