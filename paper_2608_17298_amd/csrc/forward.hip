@@ -60,10 +60,14 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   __shared__ unsigned s_restart;
   // pending hits of each lane: depth rounded up to a float, alpha, and
   // (list position, Gaussian index) -- 20 bytes; the exact depth is
-  // recomputed on the rare paths that need it
+  // recomputed on the rare paths that need it.  Large rings keep the list
+  // position only (16 bytes, the index is read from the list when needed):
+  // the LDS saved raises occupancy where the ring is what limits it.
+  constexpr bool kPosOnly = KB >= 16;
   __shared__ float s_btf[KB][NT];
   __shared__ double s_balpha[KB][NT];
-  __shared__ uint2 s_bpid[KB][NT];
+  __shared__ uint32_t s_bpos[KB][NT];
+  __shared__ uint32_t s_bid[kPosOnly ? 1 : KB][kPosOnly ? 1 : NT];
 
   const int n_tiles = A.tiles_x * A.tiles_y;
   const int tile = xcd_tile(blockIdx.x, n_tiles, A.tiles_x);
@@ -83,6 +87,11 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
 
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
+  // Gaussian index of ring entry s
+  auto entry_id = [&](int s) -> uint32_t {
+    if constexpr (kPosOnly) return A.pair_prim[beg + s_bpos[s][tid]];
+    else return s_bid[s][tid];
+  };
 
   double T = 1.0, L0 = 0.0, L1 = 0.0, L2 = 0.0;
   bool done = !valid;     // terminated (or no pixel)
@@ -132,7 +141,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   auto before_entry = [&](double tau, float tu, uint32_t id, int s) {
     const float st = s_btf[s][tid];
     if (tu != st) return tu < st;
-    const uint32_t sid = s_bpid[s][tid].y;
+    const uint32_t sid = entry_id(s);
     return key_less(tau, id, exact_tau(sid), sid);
   };
 
@@ -146,21 +155,22 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
       const int t = (s + 1) & (KB - 1);
       s_btf[t][tid] = s_btf[s][tid];
       s_balpha[t][tid] = s_balpha[s][tid];
-      s_bpid[t][tid] = s_bpid[s][tid];
+      s_bpos[t][tid] = s_bpos[s][tid];
+      if constexpr (!kPosOnly) s_bid[t][tid] = s_bid[s][tid];
       --j;
     }
     const int t = (head + j) & (KB - 1);
     s_btf[t][tid] = tu;
     s_balpha[t][tid] = a;
-    s_bpid[t][tid] = make_uint2(cpos, id);
+    s_bpos[t][tid] = cpos;
+    if constexpr (!kPosOnly) s_bid[t][tid] = id;
     if (j == 0) head_tf = tu;
     ++cnt;
   };
 
   auto composite_front = [&]() {
     const double a = s_balpha[head][tid];
-    const uint2 pid = s_bpid[head][tid];
-    const uint32_t cpos = pid.x, id = pid.y;
+    const uint32_t cpos = s_bpos[head][tid], id = entry_id(head);
     const float* shp = A.sh + int64_t(id) * (3 * K);
     const int4 rr = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
     const int64_t e = A.lt_offset[id] + lt_local_index(rr.x, rr.y, rr.z, rr.w, TILE, px, py);
@@ -257,7 +267,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
             } else {
               // the tail's depth is above the float below its rounded-up bound
               const float tf = s_btf[s][tid];  // > 0 (a hit has tau > 0)
-              drop(double(__uint_as_float(__float_as_uint(tf) - 1u)), s_bpid[s][tid].x);
+              drop(double(__uint_as_float(__float_as_uint(tf) - 1u)), s_bpos[s][tid]);
               cnt = KB - 1;
             }
           }
