@@ -180,6 +180,9 @@ typedef struct {
                              for tile t with pairs [b, e) (tile_range), the k-th composited hit of
                              pixel q of the tile (row-major) is list position (pair - b), stored at
                              hit_list[tile^2 * (b + k) + q]; k < n_hits <= e - b */
+  int64_t hit_list_capacity; /* number of uint32 slots allocated for hit_list; gart_forward and
+                             gart_backward return GART_ERR_CAPACITY if it is below
+                             pair_count * tile^2 */
   /* scratch for sorting and gradient accumulation, size from gart_scratch_bytes */
   void* scratch;
   size_t scratch_bytes;

@@ -162,6 +162,15 @@ gart_status check_frame_geometry(const gart_frame* f, const gart_camera* c, cons
   return GART_OK;
 }
 
+// hit_list holds tile^2 slots per pair (see gart_frame.hit_list).
+gart_status check_hit_list_capacity(const gart_frame* f) {
+  const int64_t need = f->pair_count * int64_t(f->tile) * f->tile;
+  if (need > f->hit_list_capacity)
+    return fail(GART_ERR_CAPACITY, "hit_list needs %lld slots (have %lld)", (long long)need,
+                (long long)f->hit_list_capacity);
+  return GART_OK;
+}
+
 // Scratch regions of the bounds step, wherever they live (the frame's
 // scratch, or the library's static array).
 struct BoundsScratch {
@@ -473,6 +482,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   GART_REQUIRE(f->lt_entries <= f->lt_capacity, "lt capacity");
   GART_REQUIRE(f->lt_entries == 0 || (f->lt != nullptr && aligned16(f->lt)), "lt must be non-NULL, 16-byte aligned");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
+  if ((st = check_hit_list_capacity(f)) != GART_OK) return st;
   const int Kf = (f->sh_degree + 1) * (f->sh_degree + 1);
   const Layout Lf = make_layout(f->n, Kf, f->pair_capacity, settings->backward_mode, settings->tile);
   GART_REQUIRE(f->scratch != nullptr && f->scratch_bytes >= Lf.total, "scratch_bytes %zu < required %zu",
@@ -524,6 +534,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
+  if ((st = check_hit_list_capacity(f)) != GART_OK) return st;
   GART_REQUIRE(f->lt_format == lt_format_for(settings),
                "frame lt_format %d does not match backward mode %d / lt_precision %d (render with the same settings)",
                f->lt_format, settings->backward_mode, settings->lt_precision);

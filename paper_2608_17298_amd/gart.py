@@ -72,6 +72,7 @@ class gart_frame(ctypes.Structure):
     _fields_ = [("rect", _P), ("lt_offset", _P), ("prim_geom", _P), ("tile_count", _P),
                 ("pair_offset", _P), ("pair_capacity", ctypes.c_int64), ("pair_tile", _P), ("pair_prim", _P),
                 ("pair_key", _P), ("tile_range", _P), ("lt_capacity", ctypes.c_int64), ("lt", _P), ("pixel_state", _P), ("hit_list", _P),
+                ("hit_list_capacity", ctypes.c_int64),
                 ("scratch", _P), ("scratch_bytes", ctypes.c_size_t), ("counters", _P),
                 ("events", _P * 8), ("n", ctypes.c_int64), ("sh_degree", ctypes.c_int32), ("tiles_x", ctypes.c_int32),
                 ("tiles_y", ctypes.c_int32), ("lt_entries", ctypes.c_int64), ("pair_count", ctypes.c_int64),
@@ -300,6 +301,7 @@ class Frame:
         f.pair_key = _ptr(self.pair_key)
         f.lt_capacity = self.lt_capacity
         f.lt, f.pixel_state, f.hit_list = _ptr(self.lt), _ptr(self.pixel_state), _ptr(self.hit_list)
+        f.hit_list_capacity = 0 if self.hit_list is None else self.hit_list.numel()
         f.scratch, f.scratch_bytes = _ptr(self.scratch), self.scratch.numel()
         f.counters = _ptr(self.counters)
         for k in range(NUM_EVENTS):

@@ -174,6 +174,32 @@ def test_frame_geometry_checked_on_host(lib, call, change):
     assert "gart_bounds" in msg or "tile grid" in msg, msg
 
 
+@pytest.mark.parametrize("call", ["forward", "backward"])
+def test_hit_list_capacity_checked_on_host(lib, call):
+    """hit_list needs tile^2 slots per pair: a frame whose hit_list_capacity
+    is short of pair_count * tile^2 is refused with GART_ERR_CAPACITY before
+    anything is launched (stage, pair count and pointers set by hand, no GPU)."""
+    cam, st, g, f = _structs(tile=8, w=16, h=16)
+    f.stage = 3
+    f.width, f.height, f.tile = 16, 16, 8
+    f.tiles_x = f.tiles_y = 2
+    f.lt_format = 0
+    f.pair_count = 5
+    # pointers are never dereferenced: the check fails first
+    f.hit_list = f.pixel_state = ctypes.c_void_p(256)
+    f.hit_list_capacity = 5 * 64 - 1
+    g.n = f.n = 0
+    dl = ctypes.c_float(0)
+    if call == "forward":
+        r = lib.gart_forward(ctypes.byref(g), ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f),
+                             ctypes.byref(dl), None)
+    else:
+        r = lib.gart_backward(ctypes.byref(g), ctypes.byref(cam), ctypes.byref(st), ctypes.byref(f),
+                              ctypes.byref(dl), None, None, None, None, None, None)
+    assert r == -2, (call, lib.gart_last_error())
+    assert "hit_list needs 320 slots (have 319)" in lib.gart_last_error().decode()
+
+
 def test_frame_status_query_validated_on_host(lib):
     """gart_frame_status (the forward's GART_FRAME_* status word) refuses a
     NULL frame or output, and a frame the forward has not run on."""
