@@ -392,24 +392,37 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
     double cax[3];
     tile_axis(A.cam, tx, ty, ts, cax);
     const double* Q = s_q[k];
-    double kmin = __builtin_huge_val(), smax = 0.0;
+    // The corner with the smallest N (c . u) / D and the one with the
+    // largest s = |R^T u| / (c . u) are chosen by cross-multiplied
+    // comparisons (D, c . u > 0), so that one division (and one square root)
+    // per pair forms each value; a choice off by rounding moves the value by
+    // about 1e-16 relative, inside the 1e-12 margin below.
+    double kn = 0.0, kd = 1.0, sw = 0.0, sc = 1.0;  // kmin = kn / kd, smax^2 = sw / sc^2
 #pragma unroll
     for (int corner = 0; corner < 4; ++corner) {
       const double a = ax[corner & 1], b = by[corner >> 1];
       const double N = fma(Q[6], a, fma(Q[7], b, Q[8]));
       const double D = fma(a, fma(Q[0], a, 2.0 * fma(Q[1], b, Q[2])), fma(b, fma(Q[3], b, 2.0 * Q[4]), Q[5]));
       const double cu = fma(cax[0], a, fma(cax[1], b, cax[2]));  // c . u
-      kmin = fmin(kmin, N * cu / D);
+      const double nc = N * cu;
+      if (corner == 0 || nc * kd < kn * D) {
+        kn = nc;
+        kd = D;
+      }
       double w2 = 0.0;  // |R^T u|^2
 #pragma unroll
       for (int r = 0; r < 3; ++r) {
         const double wr = fma(A.cam.Rt[3 * r], a, fma(A.cam.Rt[3 * r + 1], b, A.cam.Rt[3 * r + 2]));
         w2 = fma(wr, wr, w2);
       }
-      smax = fmax(smax, sqrt(w2) / cu);
+      if (corner == 0 || w2 * (sc * sc) > sw * (cu * cu)) {
+        sw = w2;
+        sc = cu;
+      }
     }
+    const double kmin = kn / kd;
     const double tk = kmin > 0.0 ? kmin - 1e-12 * kmin : 0.0;
-    const double own = Q[9] / smax * (1.0 - 1e-12);
+    const double own = Q[9] * sc / sqrt(sw) * (1.0 - 1e-12);
     const double bound = fmax(own, tk);
     A.keys[j] = (uint32_t(ty * A.tiles_x + tx) << A.key_bits) | depth_code(bound, A.key_bits);
     A.vals[j] = uint32_t(i0 + k);
