@@ -1,6 +1,7 @@
 """The fp64 oracle built with AddressSanitizer and UndefinedBehaviorSanitizer
 (g++, host code only) and driven through every C entry point the Python
-wrapper uses, on a small SH3 scene with a rotated camera, culled and
+wrapper uses (every storage model of the backward included), on a small
+SH3 scene with a rotated camera, culled and
 eye-plane-crossing Gaussians and terminating pixels: any out-of-bounds
 access, use after free, leak of the scene or undefined behaviour (overflow,
 misaligned or null access, bad shift) fails the run."""
@@ -33,6 +34,10 @@ void orc_all_hits(void*, int64_t, const int64_t*, int32_t, int32_t, int64_t*, co
 void orc_records(void*, int64_t, const int64_t*, const int64_t*, int64_t*, double*, double*);
 void orc_backward(void*, int64_t, const int64_t*, const double*, double*, double*, double*, double*, double*);
 void orc_lt_index(void*, int32_t, int64_t, const int64_t*, const int64_t*, int64_t*);
+void orc_backward_stored(void*, int64_t, const int64_t*, const double*, double*, double*, double*, double*, double*,
+                         int32_t);
+void orc_storage_round(int32_t, int64_t, const double*, double*, double);
+double orc_colour_bound(void*);
 int32_t orc_num_threads();
 }
 static double u(unsigned& s) { s = s * 1664525u + 1013904223u; return (s >> 8) * (1.0 / 16777216.0); }
@@ -89,6 +94,12 @@ int main() {
   std::vector<double> gm(3 * n), gs(3 * n), gq(4 * n), gl(n), gsh(3 * K * n);
   orc_backward(h, 0, nullptr, dl.data(), gm.data(), gs.data(), gq.data(), gl.data(), gsh.data());
   orc_backward(h, 200, pix.data() + 100, dl.data(), gm.data(), gs.data(), gq.data(), gl.data(), gsh.data());
+  for (int model = 0; model <= 5; ++model)  // every storage model of the intermediate buffer
+    orc_backward_stored(h, 0, nullptr, dl.data(), gm.data(), gs.data(), gq.data(), gl.data(), gsh.data(), model);
+  const double bound = orc_colour_bound(h);
+  std::vector<double> xs(64), rs(64);
+  for (int k = 0; k < 64; ++k) xs[k] = k == 0 ? 0.0 : std::ldexp(u(seed), -(k % 30));
+  for (int kind = 1; kind <= 3; ++kind) orc_storage_round(kind, 64, xs.data(), rs.data(), bound / 65536.0);
   std::vector<double> dirs(3 * 50), Y(16 * 50);
   for (auto& v : dirs) v = u(seed) - 0.5;
   orc_sh_basis(3, 50, dirs.data(), Y.data());
