@@ -105,7 +105,13 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
 
   int head = 0, cnt = 0;  // ring: entries head, head + 1, ... (mod KB), sorted by (depth, index)
   double e_tau = kInf;    // lower bound on the depths of dropped hits (every buffered hit is smaller)
-  float head_tf = __int_as_float(0x7f800000);  // depth bound of the ring's head (+inf if empty)
+  // The ring's head entry (depth bound, alpha, list position, index) and the
+  // tail's depth bound are kept in registers: a plain append and each
+  // compositing step then need no LDS round trip to find them.
+  float head_tf = __int_as_float(0x7f800000);  // +inf if empty
+  double head_a = 0.0;
+  uint32_t head_pos = 0, head_id = 0;
+  float tail_tf = 0.0f;                        // valid while cnt > 0
   uint32_t jr = UINT_MAX;  // first list position holding a dropped hit
   // A rescan starts the wave at the smallest jr of its lanes; a lane skips
   // the positions before its own jr (from): every hit there was composited
@@ -149,28 +155,36 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   // larger entries move up one slot, from the tail.
   auto insert = [&](double tau, float tu, uint32_t id, uint32_t cpos, double a) {
     int j = cnt;
-    while (j > 0) {
-      const int s = (head + j - 1) & (KB - 1);
-      if (!before_entry(tau, tu, id, s)) break;
-      const int t = (s + 1) & (KB - 1);
-      s_btf[t][tid] = s_btf[s][tid];
-      s_balpha[t][tid] = s_balpha[s][tid];
-      s_bpos[t][tid] = s_bpos[s][tid];
-      if constexpr (!kPosOnly) s_bid[t][tid] = s_bid[s][tid];
-      --j;
+    if (cnt > 0 && !(tu > tail_tf)) {  // not above the tail: find the place from the tail down
+      while (j > 0) {
+        const int s = (head + j - 1) & (KB - 1);
+        if (!before_entry(tau, tu, id, s)) break;
+        const int t = (s + 1) & (KB - 1);
+        s_btf[t][tid] = s_btf[s][tid];
+        s_balpha[t][tid] = s_balpha[s][tid];
+        s_bpos[t][tid] = s_bpos[s][tid];
+        if constexpr (!kPosOnly) s_bid[t][tid] = s_bid[s][tid];
+        --j;
+      }
     }
     const int t = (head + j) & (KB - 1);
     s_btf[t][tid] = tu;
     s_balpha[t][tid] = a;
     s_bpos[t][tid] = cpos;
     if constexpr (!kPosOnly) s_bid[t][tid] = id;
-    if (j == 0) head_tf = tu;
+    if (j == cnt) tail_tf = tu;
+    if (j == 0) {
+      head_tf = tu;
+      head_a = a;
+      head_pos = cpos;
+      head_id = id;
+    }
     ++cnt;
   };
 
   auto composite_front = [&]() {
-    const double a = s_balpha[head][tid];
-    const uint32_t cpos = s_bpos[head][tid], id = entry_id(head);
+    const double a = head_a;
+    const uint32_t cpos = head_pos, id = head_id;
     const float* shp = A.sh + int64_t(id) * (3 * K);
     const int4 rr = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
     const int64_t e = A.lt_offset[id] + lt_local_index(rr.x, rr.y, rr.z, rr.w, TILE, px, py);
@@ -215,7 +229,14 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
     }
     head = (head + 1) & (KB - 1);
     --cnt;
-    head_tf = cnt > 0 ? s_btf[head][tid] : __int_as_float(0x7f800000);
+    if (cnt > 0) {
+      head_tf = s_btf[head][tid];
+      head_a = s_balpha[head][tid];
+      head_pos = s_bpos[head][tid];
+      head_id = entry_id(head);
+    } else {
+      head_tf = __int_as_float(0x7f800000);
+    }
   };
 
   uint32_t restart = 0;
@@ -269,6 +290,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
               const float tf = s_btf[s][tid];  // > 0 (a hit has tau > 0)
               drop(double(__uint_as_float(__float_as_uint(tf) - 1u)), s_bpos[s][tid]);
               cnt = KB - 1;
+              tail_tf = s_btf[(head + KB - 2) & (KB - 1)][tid];
             }
           }
           if (ins) insert(tau, tu, id, cpos, cd.sig * exp(-0.5 * D2));
