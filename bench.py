@@ -411,8 +411,9 @@ def frame_vram(frame, sc):
                  + nb(frame.pair_offset),
                  pixel_state=nb(frame.pixel_state), tile_range=nb(frame.tile_range))
     alloc["total"] = sum(alloc.values())
-    P, E, ts = frame.pair_count, frame.lt_entries, sc.tile
-    used = dict(lt=16 * E, hit_list=4 * ts * ts * P, pairs=12 * P)
+    P, E = frame.pair_count, frame.lt_entries
+    from paper_2608_17298_amd import gart
+    used = dict(lt=16 * E, hit_list=4 * gart.gart_hit_list_slots(P, frame.camera, frame.settings), pairs=12 * P)
     return {"allocated": alloc, "used_by_workload": used,
             "torch_max_allocated": int(__import__("torch").cuda.max_memory_allocated())}
 

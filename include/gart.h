@@ -176,13 +176,16 @@ typedef struct {
   gart_lt_entry* lt;      /* [lt_capacity] (L, T) in front of each composited hit, in the layout
                              frame->lt_format names (see gart_lt_format) */
   gart_pixel_state* pixel_state; /* [height*width] per-pixel end marker (see gart_pixel_state) */
-  uint32_t* hit_list;     /* [pair_capacity * tile^2] composited hits of each pixel, front to back:
+  uint32_t* hit_list;     /* [hit_list_capacity] composited hits of each pixel, front to back:
                              for tile t with pairs [b, e) (tile_range), the k-th composited hit of
                              pixel q of the tile (row-major) is list position (pair - b), stored at
-                             hit_list[tile^2 * (b + k) + q]; k < n_hits <= e - b */
+                             hit_list[tile^2 * (o_t + k) + q]; tile t owns rows [o_t, o_t + r_t)
+                             with r_t = min(e - b, k_max), k_max the most hits a pixel can
+                             composite (see gart_hit_list_slots), o_t their running sum (kept in
+                             the frame's scratch) */
   int64_t hit_list_capacity; /* number of uint32 slots allocated for hit_list; gart_forward and
                              gart_backward return GART_ERR_CAPACITY if it is below
-                             pair_count * tile^2 */
+                             gart_hit_list_slots(pair_count, ...) */
   /* scratch for sorting and gradient accumulation, size from gart_scratch_bytes */
   void* scratch;
   size_t scratch_bytes;
@@ -227,9 +230,13 @@ enum {
 /* Bits of the frame status word (see gart_frame_status). */
 enum {
   GART_FRAME_STATUS_OK = 0,
-  GART_FRAME_FORWARD_INCOMPLETE = 1 /* the forward stopped tracing a tile at its safety limit on list
+  GART_FRAME_FORWARD_INCOMPLETE = 1, /* the forward stopped tracing a tile at its safety limit on list
                                        passes: image, intermediate buffer, hit_list and pixel_state of
                                        that tile are incomplete (a library defect; never expected) */
+  GART_FRAME_HIT_LIST_FULL = 2       /* a pixel composited more hits than its tile's hit_list rows
+                                       (see gart_hit_list_slots); its last row holds the last such hit
+                                       and the backward misses the others (a library defect; never
+                                       expected) */
 };
 
 enum {
@@ -243,6 +250,15 @@ enum {
   GART_EV_REDUCE_END = 7,
   GART_NUM_EVENTS = 8
 };
+
+/* Slots (uint32) that frame->hit_list needs for pair_count (tile, Gaussian)
+ * pairs on this camera and settings: tile^2 per row, min(pairs, tiles x
+ * k_max) rows, where k_max = floor(ln t_min / ln(1 - alpha_min)) + 3 bounds
+ * the hits one pixel composites: every composited hit has alpha >= alpha_min
+ * (Sec. 3.4, Eq. 10) and compositing stops after the first hit that takes T
+ * below t_min (Sec. 5.2).  Returns -1 on invalid arguments (message from
+ * gart_last_error). */
+int64_t gart_hit_list_slots(int64_t pair_count, const gart_camera* camera, const gart_settings* settings);
 
 /* Bytes per intermediate-buffer entry that gart_forward writes for these
  * settings: 16 (GART_LT_FULL), 4 (GART_LT_T_ONLY), 8 (GART_LT_HALF,

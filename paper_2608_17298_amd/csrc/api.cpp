@@ -43,10 +43,11 @@ gart_status fail(gart_status s, const char* fmt, ...) {
 size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, status, acc, rows, row_flag, total;
+  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, status, hl_off, acc, rows, row_flag,
+      total;
 };
 
-Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
+Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile, int64_t n_tiles) {
   Layout L{};
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -58,10 +59,12 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile) {
   L.pair_key_alt = take(pc * 4);
   L.pair_val_alt = take(pc * 4);
   L.radix_tmp = take(radix_tmp_bytes(std::max(nn, pc)));
-  L.scan_tmp = take(scan_tmp_bytes(nn + 1));
+  const int64_t nt = std::max<int64_t>(n_tiles, 1);
+  L.scan_tmp = take(scan_tmp_bytes(std::max(nn, nt) + 1));
   L.totals = take(64);
   L.partials = take(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
   L.status = take(4);
+  L.hl_off = take(size_t(nt + 1) * 8);  // first hit_list row of each tile
   const size_t AS = size_t(acc_stride(K));
   const bool rows = mode == GART_BACKWARD_GATHER || mode == GART_BACKWARD_GATHER_WAVE || mode == GART_BACKWARD_HYBRID;
   L.acc = take(rows ? 4 : size_t(nn) * AS * 4);
@@ -162,9 +165,28 @@ gart_status check_frame_geometry(const gart_frame* f, const gart_camera* c, cons
   return GART_OK;
 }
 
-// hit_list holds tile^2 slots per pair (see gart_frame.hit_list).
-gart_status check_hit_list_capacity(const gart_frame* f) {
-  const int64_t need = f->pair_count * int64_t(f->tile) * f->tile;
+// Composited hits one pixel can have: each has alpha >= alpha_min (the hit
+// criterion) and compositing stops after the first hit that takes T below
+// t_min, so before the last hit T >= t_min while T <= (1 - alpha_min)^(k-1):
+// k <= 1 + ln(t_min) / ln(1 - alpha_min).  alpha_min is lowered by 1e-9
+// relative and 2 added against the rounding of alpha and of the products.
+int64_t hit_rows_cap(const gart_settings* st) {
+  const double a = double(st->alpha_min), t = double(st->t_min);
+  if (!(a > 0.0 && a < 1.0 && t > 0.0 && t < 1.0)) return INT64_MAX;
+  const double k = std::floor(std::log(t) / std::log1p(-a * (1.0 - 1e-9))) + 3.0;
+  return k < 1e15 ? int64_t(k) : INT64_MAX;
+}
+
+// hit_list slots a frame needs: tile^2 per row, each tile's rows its list
+// length capped at hit_rows_cap.
+int64_t hit_list_slots(int64_t pair_count, int64_t n_tiles, int tile, const gart_settings* st) {
+  const int64_t cap = hit_rows_cap(st);
+  const int64_t rows = (cap == INT64_MAX || n_tiles > pair_count / cap) ? pair_count : n_tiles * cap;
+  return std::min(pair_count, rows) * int64_t(tile) * tile;
+}
+
+gart_status check_hit_list_capacity(const gart_frame* f, const gart_settings* st) {
+  const int64_t need = hit_list_slots(f->pair_count, int64_t(f->tiles_x) * f->tiles_y, f->tile, st);
   if (need > f->hit_list_capacity)
     return fail(GART_ERR_CAPACITY, "hit_list needs %lld slots (have %lld)", (long long)need,
                 (long long)f->hit_list_capacity);
@@ -348,7 +370,8 @@ gart_status gart_frame_status(const gart_frame* f, uint32_t* flags_host, void* s
   GART_REQUIRE(f->stage >= 3, "gart_forward has not run on this frame");
   const int K = (f->sh_degree + 1) * (f->sh_degree + 1);
   // the status word's offset does not depend on the backward mode
-  const Layout L = make_layout(f->n, K, f->pair_capacity, GART_BACKWARD_GATHER, f->tile);
+  const Layout L = make_layout(f->n, K, f->pair_capacity, GART_BACKWARD_GATHER, f->tile,
+                               int64_t(f->tiles_x) * f->tiles_y);
   GART_REQUIRE(f->scratch != nullptr && f->scratch_bytes >= L.status + 4, "frame scratch is too small");
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint32_t v = 0;
@@ -356,6 +379,18 @@ gart_status gart_frame_status(const gart_frame* f, uint32_t* flags_host, void* s
   GART_HIP(hipStreamSynchronize(s));
   *flags_host = v;
   return GART_OK;
+}
+
+int64_t gart_hit_list_slots(int64_t pair_count, const gart_camera* camera, const gart_settings* settings) {
+  g_err[0] = 0;
+  if (check_camera(camera) != GART_OK || check_settings(settings) != GART_OK) return -1;
+  if (pair_count < 0) {
+    fail(GART_ERR_INVALID_ARG, "pair_count %lld < 0", (long long)pair_count);
+    return -1;
+  }
+  const int64_t n_tiles =
+      int64_t(tiles_along(camera->width, settings->tile)) * tiles_along(camera->height, settings->tile);
+  return hit_list_slots(pair_count, n_tiles, settings->tile, settings);
 }
 
 int32_t gart_lt_entry_bytes(const gart_settings* settings) {
@@ -367,11 +402,14 @@ int32_t gart_lt_entry_bytes(const gart_settings* settings) {
 
 size_t gart_scratch_bytes(int64_t n, int32_t sh_degree, int64_t pair_capacity, const gart_camera* camera,
                           const gart_settings* settings) {
-  (void)camera;
   const int deg = std::min(std::max(sh_degree, 0), 3);
   const int mode = settings ? settings->backward_mode : GART_BACKWARD_GATHER;
-  return make_layout(std::max<int64_t>(n, 0), (deg + 1) * (deg + 1), std::max<int64_t>(pair_capacity, 0), mode,
-                     settings && settings->tile == 16 ? 16 : 8)
+  const int tile = settings && settings->tile == 16 ? 16 : 8;
+  const int64_t n_tiles = camera && camera->width > 0 && camera->height > 0
+                              ? int64_t(tiles_along(camera->width, tile)) * tiles_along(camera->height, tile)
+                              : 1;
+  return make_layout(std::max<int64_t>(n, 0), (deg + 1) * (deg + 1), std::max<int64_t>(pair_capacity, 0), mode, tile,
+                     n_tiles)
       .total;
 }
 
@@ -383,7 +421,9 @@ gart_status gart_bounds(const gart_gaussians* g, const gart_camera* camera, cons
   const int64_t n = g->n;
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
   GART_REQUIRE(f->scratch != nullptr, "frame scratch is NULL");
-  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile);
+  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile,
+                               int64_t(tiles_along(camera->width, settings->tile)) *
+                                   tiles_along(camera->height, settings->tile));
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
   BoundsScratch S;
   S.scan_tmp = at<void>(f->scratch, L.scan_tmp);
@@ -426,7 +466,7 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   GART_REQUIRE(P <= f->pair_capacity, "pair capacity");
   if (P > 0) GART_REQUIRE(f->pair_tile && f->pair_prim && f->pair_key, "frame pair buffers are NULL");
   const int K = (f->sh_degree + 1) * (f->sh_degree + 1);
-  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile);
+  const Layout L = make_layout(n, K, f->pair_capacity, settings->backward_mode, settings->tile, n_tiles);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu", f->scratch_bytes, L.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
@@ -463,6 +503,11 @@ gart_status gart_build_tile_map(const gart_camera* camera, const gart_settings* 
   GART_HIP(record(f->events[GART_EV_SORT_END], s));
   T.keys = f->pair_tile;
   GART_HIP(launch_finish_pairs(T, sorted_keys, n_tiles, s));
+  // hit_list rows of each tile: its list length, at most the hits a pixel can
+  // composite; offsets by an exclusive scan
+  int64_t* hl_off = at<int64_t>(f->scratch, L.hl_off);
+  GART_HIP(launch_hit_rows(f->tile_range, n_tiles, hit_rows_cap(settings), hl_off, s));
+  GART_HIP(scan_exclusive_i64(hl_off, hl_off, n_tiles, hl_off + n_tiles, at<void>(f->scratch, L.scan_tmp), s));
   f->stage = 2;
   return GART_OK;
 }
@@ -482,9 +527,10 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   GART_REQUIRE(f->lt_entries <= f->lt_capacity, "lt capacity");
   GART_REQUIRE(f->lt_entries == 0 || (f->lt != nullptr && aligned16(f->lt)), "lt must be non-NULL, 16-byte aligned");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
-  if ((st = check_hit_list_capacity(f)) != GART_OK) return st;
+  if ((st = check_hit_list_capacity(f, settings)) != GART_OK) return st;
   const int Kf = (f->sh_degree + 1) * (f->sh_degree + 1);
-  const Layout Lf = make_layout(f->n, Kf, f->pair_capacity, settings->backward_mode, settings->tile);
+  const Layout Lf = make_layout(f->n, Kf, f->pair_capacity, settings->backward_mode, settings->tile,
+                                int64_t(f->tiles_x) * f->tiles_y);
   GART_REQUIRE(f->scratch != nullptr && f->scratch_bytes >= Lf.total, "scratch_bytes %zu < required %zu",
                f->scratch_bytes, Lf.total);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -508,6 +554,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.image = image;
   A.pixel_state = f->pixel_state;
   A.hit_list = f->hit_list;
+  A.hl_off = at<int64_t>(f->scratch, Lf.hl_off);
   A.counters = f->counters;
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
@@ -534,13 +581,14 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   GART_REQUIRE(g->n == f->n && g->sh_degree == f->sh_degree, "gaussians differ from gart_bounds");
   GART_REQUIRE(dL_dimage != nullptr, "dL_dimage is NULL");
   GART_REQUIRE(f->pair_count == 0 || f->hit_list != nullptr, "hit_list is NULL");
-  if ((st = check_hit_list_capacity(f)) != GART_OK) return st;
+  if ((st = check_hit_list_capacity(f, settings)) != GART_OK) return st;
   GART_REQUIRE(f->lt_format == lt_format_for(settings),
                "frame lt_format %d does not match backward mode %d / lt_precision %d (render with the same settings)",
                f->lt_format, settings->backward_mode, settings->lt_precision);
   if (g->n > 0) GART_REQUIRE(g_means && g_log_scales && g_quats && g_logits && g_sh, "gradient pointer is NULL");
   const int K = (g->sh_degree + 1) * (g->sh_degree + 1);
-  const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode, settings->tile);
+  const Layout L = make_layout(f->n, K, f->pair_capacity, settings->backward_mode, settings->tile,
+                               int64_t(f->tiles_x) * f->tiles_y);
   GART_REQUIRE(f->scratch_bytes >= L.total, "scratch_bytes %zu < required %zu (backward mode %d)", f->scratch_bytes,
                L.total, settings->backward_mode);
   GART_REQUIRE(aligned16(f->scratch), "scratch must be 16-byte aligned");
@@ -568,6 +616,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.dl_dimage = dL_dimage;
   A.pixel_state = f->pixel_state;
   A.hit_list = f->hit_list;
+  A.hl_off = at<int64_t>(f->scratch, L.hl_off);
   A.acc = at<float>(f->scratch, L.acc);
   A.rows = at<float>(f->scratch, L.rows);
   A.row_flag = at<uint8_t>(f->scratch, L.row_flag);

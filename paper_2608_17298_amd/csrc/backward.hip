@@ -335,7 +335,7 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
     // issued eight at a time).
     {
       const uint32_t lo = uint32_t(c0 - beg);
-      const uint32_t* hl = A.hit_list + int64_t(NT) * beg + tid;
+      const uint32_t* hl = A.hit_list + int64_t(NT) * A.hl_off[tile] + tid;
       const uint64_t bit = 1ull << (tid % 64);
       uint32_t k = 0;
       for (; k + 8 <= my_hits; k += 8) {
@@ -591,7 +591,7 @@ __global__ __launch_bounds__(TILE* TILE) void hybrid_pixel_kernel(BackwardArgs A
     nh = int(A.pixel_state[p].n_hits);
   }
   const int64_t beg = A.tile_range[tile];
-  const uint32_t* hl = A.hit_list + int64_t(NT) * beg + tid;
+  const uint32_t* hl = A.hit_list + int64_t(NT) * A.hl_off[tile] + tid;
   uint32_t n_walk = 0;
 
   for (int w0 = 0;; w0 += kWin) {

@@ -447,7 +447,19 @@ __global__ void finish_pairs_kernel(TileMapArgs A, const uint32_t* __restrict__ 
   for (int64_t t = prev + 1; t <= cur && t <= n_tiles; ++t) A.tile_range[t] = j;
 }
 
+__global__ void hit_rows_kernel(const int64_t* __restrict__ tile_range, int64_t n_tiles, int64_t cap,
+                                int64_t* __restrict__ rows) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t < n_tiles) rows[t] = min(tile_range[t + 1] - tile_range[t], cap);
+}
+
 }  // namespace
+
+hipError_t launch_hit_rows(const int64_t* tile_range, int64_t n_tiles, int64_t cap, int64_t* rows, hipStream_t s) {
+  if (n_tiles <= 0) return hipSuccess;
+  hit_rows_kernel<<<ceil_div(n_tiles, 256), 256, 0, s>>>(tile_range, n_tiles, cap, rows);
+  return hipGetLastError();
+}
 
 hipError_t launch_bounds(const BoundsArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;

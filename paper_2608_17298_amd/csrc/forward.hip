@@ -87,6 +87,11 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   sh_basis<K>(float(d[0]), float(d[1]), float(d[2]), Y);
 
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
+  const int64_t hl_beg = A.hl_off[tile];  // this tile's first hit_list row
+  // its rows (>= 1 if the tile has pairs); a hit beyond them, which the
+  // bound on hits per pixel excludes, would overwrite the last row and is
+  // reported in the frame status after the trace
+  const uint32_t hl_last = uint32_t(max<int64_t>(A.hl_off[tile + 1] - hl_beg, 1) - 1);
   // Gaussian index of ring entry s
   auto entry_id = [&](int s) -> uint32_t {
     if constexpr (kPosOnly) return A.pair_prim[beg + s_bpos[s][tid]];
@@ -197,7 +202,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
     for (int ch = 0; ch < 3; ++ch) c[ch] = fmaxf(c[ch], 0.0f);
     // k-th composited hit of this pixel -> its list position (read by the
     // gather backward)
-    A.hit_list[int64_t(NT) * (beg + n_hits) + tid] = cpos;
+    A.hit_list[int64_t(NT) * (hl_beg + min(n_hits, hl_last)) + tid] = cpos;
     if constexpr (FMT == GART_LT_FULL) {
       A.lt[e] = make_uint4(color_fixed(L0, A.inv_color_step), color_fixed(L1, A.inv_color_step),
                            color_fixed(L2, A.inv_color_step), __float_as_uint(float(T)));
@@ -386,6 +391,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   }
 
   if (end_id != kNoPrim) end_tau = exact_tau(end_id);
+  if (__ballot(n_hits > hl_last + 1u) != 0 && lane_id() == 0) atomicOr(A.status, unsigned(GART_FRAME_HIT_LIST_FULL));
   if (valid) {
     const int64_t p = int64_t(py) * A.cam.W + px;
     A.image[3 * p + 0] = float(L0);

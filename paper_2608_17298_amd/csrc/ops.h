@@ -87,6 +87,9 @@ hipError_t launch_emit_pairs(const TileMapArgs& a, hipStream_t s);
 // id, a.pair_key[j] = decoded depth bound, and a.tile_range[t] = first pair
 // whose tile id is >= t, for t in [0, n_tiles].
 hipError_t launch_finish_pairs(const TileMapArgs& a, const uint32_t* sorted_keys, int64_t n_tiles, hipStream_t s);
+// rows[t] = min(tile_range[t+1] - tile_range[t], cap): the hit_list rows of
+// tile t (a pixel composites at most one hit per pair and at most cap hits)
+hipError_t launch_hit_rows(const int64_t* tile_range, int64_t n_tiles, int64_t cap, int64_t* rows, hipStream_t s);
 
 // ---- forward.hip -------------------------------------------------------
 struct ForwardArgs {
@@ -105,7 +108,8 @@ struct ForwardArgs {
   double inv_color_step;    // fixed-point units per unit of colour
   float* image;
   gart_pixel_state* pixel_state;
-  uint32_t* hit_list;       // [pairs * tile^2] list position of each pixel's k-th composited hit
+  uint32_t* hit_list;       // list position of each pixel's k-th composited hit, at row hl_off[tile] + k
+  const int64_t* hl_off;    // [n_tiles+1] first hit_list row of each tile (tile^2 slots per row)
   uint32_t* status;         // frame status word (GART_FRAME_* bits), cleared before the launch
   int64_t pair_count;       // pairs in the tile lists (sizes the per-lane pending-hit rings)
   uint64_t* counters;
@@ -133,7 +137,8 @@ struct BackwardArgs {
   float color_step;         // colour per fixed-point unit (a power of two times a float)
   const float* dl_dimage;
   const gart_pixel_state* pixel_state;
-  const uint32_t* hit_list;  // [pairs * tile^2] list position of each pixel's k-th composited hit
+  const uint32_t* hit_list;  // list position of each pixel's k-th composited hit, at row hl_off[tile] + k
+  const int64_t* hl_off;     // [n_tiles+1] first hit_list row of each tile (tile^2 slots per row)
   // gradient accumulation
   float* acc;          // [n, acc_stride] per-Gaussian accumulators (atomic modes)
   float* rows;         // [P * rows_per_pair, acc_stride] partial rows (gather mode)

@@ -108,6 +108,8 @@ def lib():
         L.gart_scratch_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int64, _P, _P]
         L.gart_lt_entry_bytes.restype = ctypes.c_int32
         L.gart_lt_entry_bytes.argtypes = [_P]
+        L.gart_hit_list_slots.restype = ctypes.c_int64
+        L.gart_hit_list_slots.argtypes = [ctypes.c_int64, _P, _P]
         L.gart_bounds.restype = ctypes.c_int
         L.gart_bounds.argtypes = [_P, _P, _P, _P, _P, _P, _P]
         L.gart_bounds_noalloc.restype = ctypes.c_int
@@ -227,6 +229,13 @@ class Gaussians:
         return g
 
 
+def gart_hit_list_slots(pair_count, camera: gart_camera, settings: gart_settings) -> int:
+    r = int(lib().gart_hit_list_slots(int(pair_count), ctypes.byref(camera), ctypes.byref(settings)))
+    if r < 0:
+        raise GartError(GART_ERR_INVALID_ARG, "gart_hit_list_slots", lib().gart_last_error().decode())
+    return r
+
+
 def gart_scratch_bytes(n, sh_degree, pair_capacity, camera: gart_camera, settings: gart_settings) -> int:
     return int(lib().gart_scratch_bytes(int(n), int(sh_degree), int(pair_capacity), ctypes.byref(camera),
                                         ctypes.byref(settings)))
@@ -273,8 +282,9 @@ class Frame:
         self.pair_tile = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
         self.pair_prim = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
         self.pair_key = torch.empty(max(cap, 1), dtype=torch.float32, device=self.device)
-        # composited-hit lists: tile^2 slots per pair (see gart_frame.hit_list)
-        self.hit_list = torch.empty(max(cap, 1) * self.settings.tile ** 2, dtype=torch.int32, device=self.device)
+        # composited-hit lists (see gart_frame.hit_list)
+        self.hit_list = torch.empty(max(gart_hit_list_slots(cap, self.camera, self.settings), 1), dtype=torch.int32,
+                                    device=self.device)
         self.pair_capacity = cap
         # sized for every backward mode, so one frame serves all of them
         nbytes = 0
@@ -393,6 +403,7 @@ def gart_bounds_noalloc(g: Gaussians, camera: gart_camera, settings: gart_settin
 
 
 FRAME_FORWARD_INCOMPLETE = 1
+FRAME_HIT_LIST_FULL = 2
 
 
 def gart_frame_status(frame: Frame, stream=None) -> int:

@@ -200,6 +200,30 @@ def test_hit_list_capacity_checked_on_host(lib, call):
     assert "hit_list needs 320 slots (have 319)" in lib.gart_last_error().decode()
 
 
+def test_hit_list_slots(lib):
+    """gart_hit_list_slots: tile^2 slots per pair while the pairs are fewer
+    than (tiles x k_max), then tiles x k_max rows, where k_max is the most
+    hits a pixel can composite: the smallest k with (1 - alpha_min)^(k - 1)
+    below t_min, plus a small guard; -1 for invalid arguments."""
+    import math
+    from paper_2608_17298_amd import gart
+    cam, st, g, f = _structs(tile=8, w=57, h=43)  # 8 x 6 tiles
+    n_tiles = 48
+    a, t = float(st.alpha_min), float(st.t_min)  # float32 settings, read back as doubles
+    k_lo = 1 + math.floor(math.log(t) / math.log(1 - a))  # hits a pixel can actually reach
+    assert gart.gart_hit_list_slots(0, cam, st) == 0
+    assert gart.gart_hit_list_slots(1000, cam, st) == 1000 * 64
+    big = gart.gart_hit_list_slots(10 ** 9, cam, st)
+    assert big % (64 * n_tiles) == 0
+    k_max = big // (64 * n_tiles)
+    assert k_lo <= k_max <= k_lo + 3, (k_lo, k_max)
+    st16 = gart.make_settings(16, 0)  # 4 x 3 tiles of 256 pixels
+    assert gart.gart_hit_list_slots(10 ** 9, cam, st16) == k_max * 256 * 12
+    assert lib.gart_hit_list_slots(-1, ctypes.byref(cam), ctypes.byref(st)) == -1
+    st.alpha_min = 0.0
+    assert lib.gart_hit_list_slots(10, ctypes.byref(cam), ctypes.byref(st)) == -1
+
+
 def test_frame_status_query_validated_on_host(lib):
     """gart_frame_status (the forward's GART_FRAME_* status word) refuses a
     NULL frame or output, and a frame the forward has not run on."""
