@@ -43,8 +43,8 @@ gart_status fail(gart_status s, const char* fmt, ...) {
 size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, status, hl_off, acc, rows, row_flag,
-      total;
+  size_t pair_key_alt, pair_val_alt, radix_tmp, scan_tmp, totals, partials, status, hl_off, tile_visit, acc, rows,
+      row_flag, total;
 };
 
 Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile, int64_t n_tiles) {
@@ -65,6 +65,7 @@ Layout make_layout(int64_t n, int K, int64_t pair_cap, int mode, int tile, int64
   L.partials = take(size_t((nn + kBoundsBlock - 1) / kBoundsBlock) * 16);
   L.status = take(4);
   L.hl_off = take(size_t(nt + 1) * 8);  // first hit_list row of each tile
+  L.tile_visit = take(size_t(nt) * 4);  // the forward's visited prefix of each tile's list
   const size_t AS = size_t(acc_stride(K));
   const bool rows = mode == GART_BACKWARD_GATHER || mode == GART_BACKWARD_GATHER_WAVE || mode == GART_BACKWARD_HYBRID;
   L.acc = take(rows ? 4 : size_t(nn) * AS * 4);
@@ -555,6 +556,7 @@ gart_status gart_forward(const gart_gaussians* g, const gart_camera* camera, con
   A.pixel_state = f->pixel_state;
   A.hit_list = f->hit_list;
   A.hl_off = at<int64_t>(f->scratch, Lf.hl_off);
+  A.tile_visit = at<uint32_t>(f->scratch, Lf.tile_visit);
   A.counters = f->counters;
   A.ev_begin = f->events[GART_EV_FWD_BEGIN];
   A.ev_end = f->events[GART_EV_FWD_END];
@@ -617,6 +619,7 @@ gart_status gart_backward(const gart_gaussians* g, const gart_camera* camera, co
   A.pixel_state = f->pixel_state;
   A.hit_list = f->hit_list;
   A.hl_off = at<int64_t>(f->scratch, L.hl_off);
+  A.tile_visit = at<uint32_t>(f->scratch, L.tile_visit);
   A.acc = at<float>(f->scratch, L.acc);
   A.rows = at<float>(f->scratch, L.rows);
   A.row_flag = at<uint8_t>(f->scratch, L.row_flag);

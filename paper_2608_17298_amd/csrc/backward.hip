@@ -247,8 +247,6 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
   __shared__ uint32_t s_total;
   __shared__ uint32_t s_dense;
   __shared__ uint32_t s_split;
-  __shared__ double s_wmax[G];
-  __shared__ uint32_t s_red[G];
   __shared__ uint64_t s_mask[kUnits];
   __shared__ uint32_t s_id[kPairs];
   __shared__ uint8_t s_bucket[kUnits];
@@ -271,7 +269,6 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
     for (int k = 0; k < KP; ++k) s_Y[tid][k] = k < K ? Y[k] : 0.0f;
     uint32_t cq[3] = {0, 0, 0};
     float gg[3] = {0, 0, 0};
-    double tend = -__builtin_huge_val();
     if (valid) {
       const int64_t p = int64_t(py) * A.cam.W + px;
 #pragma unroll
@@ -280,7 +277,6 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
         cq[ch] = A.pixel_state[p].color_fixed[ch];
       }
       my_hits = A.pixel_state[p].n_hits;
-      tend = A.pixel_state[p].tau_end;
     }
     RayRec rr;
     rr.d[0] = d[0];
@@ -290,35 +286,13 @@ __global__ __launch_bounds__(TILE* TILE, 2) void gather_kernel(BackwardArgs A) {
     s_ray[tid] = rr;
     *reinterpret_cast<uint4*>(&s_cg[tid][0]) = make_uint4(cq[0], cq[1], cq[2], __float_as_uint(gg[0]));
     *reinterpret_cast<float4*>(&s_cg[tid][4]) = make_float4(gg[1], gg[2], 0.0f, 0.0f);
-    // the latest ray end in the tile's key units (a key k bounds a hit's
-    // depth on this ray by k * key_scale), rounded up
-    double cax[3];
-    tile_axis(A.cam, tx, ty, TILE, cax);
-    double m = tend / key_scale(A.cam, cax, valid ? px : 0, valid ? py : 0);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
-    if (tid % 64 == 0) s_wmax[tid / 64] = m;
   }
   __syncthreads();
-  double tmax = s_wmax[0];
-#pragma unroll
-  for (int w = 1; w < G; ++w) tmax = fmax(tmax, s_wmax[w]);
 
-  // Only the prefix of the depth-ordered list whose depth bound lies in front
-  // of the tile's latest ray end can hold composited hits.
+  // Composited hits lie in the first tile_visit[tile] positions of the tile's
+  // list (the forward records one past the largest position it composited).
   const int64_t beg = A.tile_range[tile], end = A.tile_range[tile + 1];
-  uint32_t nv = 0;
-  for (int64_t j = beg + tid; j < end; j += NT) {
-    if (double(A.pair_key[j]) > tmax) break;
-    ++nv;
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) nv += __shfl_xor(nv, off);
-  if (tid % 64 == 0) s_red[tid / 64] = nv;
-  __syncthreads();
-  int64_t vend = beg;
-#pragma unroll
-  for (int w = 0; w < G; ++w) vend += s_red[w];
+  const int64_t vend = min(end, beg + int64_t(A.tile_visit[tile]));
 
   uint32_t n_pairs = 0, n_hits = 0, n_atom = 0, n_active = 0, n_wave = 0;
   for (int64_t c0 = beg; c0 < vend; c0 += kPairs) {

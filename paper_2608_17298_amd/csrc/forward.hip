@@ -103,6 +103,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   bool finished = false;  // every hit composited
   bool stalled = false;   // must wait for a rescan
   uint32_t n_hits = 0, n_tests = 0, n_drops = 0;
+  uint32_t visited = 0;  // one past the largest list position composited
   double last_tau = -kInf;
   uint32_t last_id = 0;
   double end_tau = kInf;
@@ -190,6 +191,7 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
   auto composite_front = [&]() {
     const double a = head_a;
     const uint32_t cpos = head_pos, id = head_id;
+    visited = max(visited, cpos + 1u);
     const float* shp = A.sh + int64_t(id) * (3 * K);
     const int4 rr = *reinterpret_cast<const int4*>(A.rect + 4 * int64_t(id));
     const int64_t e = A.lt_offset[id] + lt_local_index(rr.x, rr.y, rr.z, rr.w, TILE, px, py);
@@ -390,6 +392,15 @@ __global__ GART_FWD_LAUNCH_BOUNDS(TILE* TILE) void forward_kernel(ForwardArgs A)
     }
   }
 
+  // the tile's visited prefix for the backward: the block's largest
+  __shared__ uint32_t s_visited;
+  if (tid == 0) s_visited = 0;
+  __syncthreads();
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) visited = max(visited, uint32_t(__shfl_xor(int(visited), off)));
+  if (lane_id() == 0) atomicMax(&s_visited, visited);
+  __syncthreads();
+  if (tid == 0) A.tile_visit[tile] = s_visited;
   if (end_id != kNoPrim) end_tau = exact_tau(end_id);
   if (__ballot(n_hits > hl_last + 1u) != 0 && lane_id() == 0) atomicOr(A.status, unsigned(GART_FRAME_HIT_LIST_FULL));
   if (valid) {

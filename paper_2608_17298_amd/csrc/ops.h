@@ -110,6 +110,7 @@ struct ForwardArgs {
   gart_pixel_state* pixel_state;
   uint32_t* hit_list;       // list position of each pixel's k-th composited hit, at row hl_off[tile] + k
   const int64_t* hl_off;    // [n_tiles+1] first hit_list row of each tile (tile^2 slots per row)
+  uint32_t* tile_visit;     // [n_tiles] one past the largest list position composited in the tile
   uint32_t* status;         // frame status word (GART_FRAME_* bits), cleared before the launch
   int64_t pair_count;       // pairs in the tile lists (sizes the per-lane pending-hit rings)
   uint64_t* counters;
@@ -139,6 +140,7 @@ struct BackwardArgs {
   const gart_pixel_state* pixel_state;
   const uint32_t* hit_list;  // list position of each pixel's k-th composited hit, at row hl_off[tile] + k
   const int64_t* hl_off;     // [n_tiles+1] first hit_list row of each tile (tile^2 slots per row)
+  const uint32_t* tile_visit;  // [n_tiles] one past the largest list position composited (forward)
   // gradient accumulation
   float* acc;          // [n, acc_stride] per-Gaussian accumulators (atomic modes)
   float* rows;         // [P * rows_per_pair, acc_stride] partial rows (gather mode)
