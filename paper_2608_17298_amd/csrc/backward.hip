@@ -128,7 +128,8 @@ __device__ __forceinline__ float wave_sum32_transposed(float* v) {
 // (pair, group): the composited hits of one Gaussian in one group.  Per tile:
 //  1. Per-pixel state (ray direction, SH basis, final colour and upstream
 //     gradient) is staged in LDS.
-//  2. The tile's pairs are taken in LDS passes of up to kUnits units.  Each
+//  2. The tile's pairs, up to one past the largest list position the forward
+//     composited in the tile, are taken in LDS passes of up to kUnits units.  Each
 //     pixel walks the list of its composited hits that the forward recorded
 //     and sets its bit in the 64-bit mask of the unit it belongs to (LDS
 //     atomics).  Units without a composited hit are dropped, the rest are
