@@ -770,43 +770,230 @@ __global__ __launch_bounds__(TILE* TILE) void scatter_kernel(BackwardArgs A) {
 // ---------------------------------------------------------------------------
 // Per-Gaussian reduction of the pair rows (gather mode) or read of the
 // atomic accumulators, then the chain rule to the raw parameters.  A block
-// serves 64 Gaussians.  Reduction: sixteen lanes per Gaussian, lane q reads
-// float4 q of each active row (a Gaussian's rows are contiguous: its pairs in
-// emission order, rows_per_pair pixel groups each), 16
-// row flags are read at once and up to four rows are loaded per step.
+// serves 64 Gaussians, whose rows form one contiguous range (pairs are in
+// emission order, Gaussian by Gaussian, rows_per_pair pixel groups each).
+//
+// Row sums: the block reads the range's row flags in coalesced chunks, lists
+// a chunk's active rows in row order, and gives each of its sixteen lane
+// groups an equal contiguous share of the list (lane q of a group owns
+// float4 q of a row).  A group sums its share in order.  A Gaussian whose
+// rows in the chunk all lie in one share is added to its LDS row directly;
+// one cut by share boundaries is added there by its first share, and the
+// partials of the following shares are added afterwards in share order.
+// Every order depends on the flags alone, so the sums are deterministic, and
+// a Gaussian with a thousand tiles is spread over the block instead of
+// serialising one lane group.
+//
 // Chain rule: one Gaussian per lane of the first wave.  SH gradients: all
 // threads, coalesced.
 // ---------------------------------------------------------------------------
-#ifndef GART_REDUCE_BLOCK
-#define GART_REDUCE_BLOCK 256
+#ifndef GART_REDUCE_CHUNK
+#define GART_REDUCE_CHUNK 1024
 #endif
-#ifndef GART_REDUCE_GAUSSIANS
-#define GART_REDUCE_GAUSSIANS 64
-#endif
-#ifndef GART_REDUCE_LANES
-#define GART_REDUCE_LANES 16
-#endif
-constexpr int kReduceLanes = GART_REDUCE_LANES;  // lanes per Gaussian in the row sum
-constexpr int kReduceBlock = GART_REDUCE_BLOCK;
-constexpr int kReduceGaussians = GART_REDUCE_GAUSSIANS;
+constexpr int kReduceLanes = 16;  // lanes per row: 16 float4 hold the widest row (64 floats)
+constexpr int kReduceBlock = 256;
+constexpr int kReduceGaussians = 64;
+constexpr int kReduceChunk = GART_REDUCE_CHUNK;  // row flags listed per pass
+static_assert(kReduceChunk % kReduceBlock == 0 && kReduceChunk <= 65536, "chunk of whole block strides");
 
-template <int K, bool ROWS>
-__global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs A) {
-  constexpr int AS = acc_stride(K), NQ = AS / 4;
-  constexpr int GROUPS = kReduceBlock / kReduceLanes;
+__device__ const uint8_t g_zero_flag = 0;  // read in place of a row flag past the range
+
+// The block's Gaussian (0 .. nb-1) whose pair range holds `pair`: the last
+// one whose first pair is <= pair (empty ranges before it are skipped).
+__device__ __forceinline__ int gaussian_of(const int64_t* po, int nb, int64_t pair) {
+  int lo = 0, hi = nb - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (po[mid] <= pair)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  return lo;
+}
+
+template <int AS>
+__device__ __forceinline__ void sum_rows(const BackwardArgs& A, int64_t i0, int nb, float (*s_acc)[AS]) {
+  constexpr int NQ = AS / 4, GROUPS = kReduceBlock / kReduceLanes;
   constexpr int NC = (NQ + kReduceLanes - 1) / kReduceLanes;  // float4 columns per lane
-  constexpr int kFlagStep = 16;                                // row flags read per step
-  static_assert(64 % kReduceLanes == 0 && kFlagStep % kReduceLanes == 0, "lane groups inside a wave");
+  constexpr int J = kReduceChunk / kReduceBlock;             // flags per thread per chunk
+  constexpr int W = kReduceBlock / 64;
+  __shared__ int64_t s_po[kReduceGaussians + 1];
+  __shared__ uint32_t s_list[kReduceChunk];
+  __shared__ uint32_t s_cnt[J * W];
+  __shared__ __align__(16) float s_part[GROUPS][AS];  // head partial of each share
+  __shared__ int s_head_id[GROUPS], s_tail_id[GROUPS];
+  const int tid = threadIdx.x, lane = tid % 64, w = tid / 64;
+  const int grp = tid / kReduceLanes, q = tid % kReduceLanes;
+  const float4 zero4 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+
+  if (tid <= nb) s_po[tid] = A.pair_offset[i0 + tid];
+  for (int e = tid; e < kReduceGaussians * NQ; e += kReduceBlock)
+    reinterpret_cast<float4*>(&s_acc[0][0])[e] = zero4;
+  __syncthreads();
+  const int rsh = __ffs(int(A.rows_per_pair)) - 1;  // rows_per_pair is 1 or 4
+  const int64_t R0 = s_po[0] << rsh, R1 = s_po[nb] << rsh;
+  const float4* rows = reinterpret_cast<const float4*>(A.rows);
+
+  for (int64_t cb = R0; cb < R1; cb += kReduceChunk) {
+    // flags of the chunk, every load issued before any is used
+    uint32_t f[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int64_t r = cb + j * kReduceBlock + tid;
+      f[j] = *(r < R1 ? A.row_flag + r : &g_zero_flag);
+    }
+    uint64_t bal[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) bal[j] = __ballot(f[j] != 0u);
+    if (lane == 0)
+#pragma unroll
+      for (int j = 0; j < J; ++j) s_cnt[j * W + w] = uint32_t(__popcll(bal[j]));
+    __syncthreads();
+    // the list of active rows (offsets from cb), in row order: (j, wave, lane)
+    uint32_t base[J], total = 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int v = 0; v < W; ++v) {
+        const uint32_t c = s_cnt[j * W + v];
+        if (v == w) base[j] = total;
+        total += c;
+      }
+    // entry: Gaussian slot << 16 | row offset in the chunk
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      if (f[j] != 0u) {
+        const uint32_t rel = uint32_t(j * kReduceBlock + tid);
+        s_list[base[j] + __builtin_amdgcn_mbcnt_hi(uint32_t(bal[j] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[j]), 0u))] =
+            uint32_t(gaussian_of(s_po, nb, (cb + rel) >> rsh)) << 16 | rel;
+      }
+    const int L = int(total);
+    __syncthreads();
+
+    // this group's share [sb, se) of the list
+    const int sb = grp * L / GROUPS, se = (grp + 1) * L / GROUPS;
+    auto gl_at = [&](int e) { return int(s_list[e] >> 16); };
+    int gfirst = -1, glast = -1;
+    bool head_cut = false, tail_cut = false;
+    if (sb < se) {
+      gfirst = gl_at(sb);
+      glast = gl_at(se - 1);
+      head_cut = sb > 0 && gl_at(sb - 1) == gfirst;
+      tail_cut = se < L && gl_at(se) == glast;
+    }
+    if (q == 0) s_head_id[grp] = s_tail_id[grp] = -1;
+    float4 acc[NC];
+    int cur = -1;
+    auto flush = [&]() {
+      // a Gaussian continued from the previous share keeps its partial apart;
+      // any other goes to its LDS row (a tail-cut one first of all its shares)
+      const bool head = cur == gfirst && head_cut;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int col = q + c * kReduceLanes;
+        if (col >= NQ) continue;
+        if (head) {
+          reinterpret_cast<float4*>(s_part[grp])[col] = acc[c];
+        } else {
+          float4* d = reinterpret_cast<float4*>(s_acc[cur]) + col;
+          float4 t = *d;
+          t.x += acc[c].x;
+          t.y += acc[c].y;
+          t.z += acc[c].z;
+          t.w += acc[c].w;
+          *d = t;
+        }
+      }
+      if (q == 0) {
+        if (head)
+          s_head_id[grp] = cur;
+        else if (cur == glast && tail_cut)
+          s_tail_id[grp] = cur;
+      }
+    };
+    for (int e = sb; e < se; e += 4) {
+      int gu[4];
+      int64_t ru[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool ok = e + u < se;
+        const uint32_t x = ok ? s_list[e + u] : 0u;
+        ru[u] = cb + (x & 0xffffu);
+        gu[u] = ok ? int(x >> 16) : -1;
+      }
+      float4 v[4][NC];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const int col = q + c * kReduceLanes;
+          v[u][c] = (gu[u] >= 0 && col < NQ) ? rows[ru[u] * NQ + col] : zero4;
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (gu[u] < 0) break;
+        if (gu[u] != cur) {
+          if (cur >= 0) flush();
+          cur = gu[u];
+#pragma unroll
+          for (int c = 0; c < NC; ++c) acc[c] = v[u][c];
+        } else {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) {
+            acc[c].x += v[u][c].x;
+            acc[c].y += v[u][c].y;
+            acc[c].z += v[u][c].z;
+            acc[c].w += v[u][c].w;
+          }
+        }
+      }
+    }
+    if (cur >= 0) flush();
+    __syncthreads();
+
+    // A cut Gaussian's first share added its part to the LDS row and named
+    // it as its tail; that share's group adds the head partials of the
+    // following shares, in share order (the shares holding one Gaussian are
+    // consecutive).
+    {
+      const int gl = s_tail_id[grp];
+      if (gl >= 0) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const int col = q + c * kReduceLanes;
+          if (col >= NQ) continue;
+          float4* d = reinterpret_cast<float4*>(s_acc[gl]) + col;
+          float4 a = *d;
+          for (int g = grp + 1; g < GROUPS; ++g) {
+            if (s_head_id[g] != gl) continue;
+            const float4 p = reinterpret_cast<const float4*>(s_part[g])[col];
+            a.x += p.x;
+            a.y += p.y;
+            a.z += p.z;
+            a.w += p.w;
+          }
+          *d = a;
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Six waves per SIMD: 80 VGPRs, and six blocks' LDS (25 KB each) fit a CU.
+template <int K, bool ROWS>
+__global__ __launch_bounds__(kReduceBlock) __attribute__((amdgpu_waves_per_eu(6))) void reduce_chain_kernel(BackwardArgs A) {
+  constexpr int AS = acc_stride(K), NQ = AS / 4;
   __shared__ __align__(16) float s_acc[kReduceGaussians][AS];
   const int64_t i0 = int64_t(blockIdx.x) * kReduceGaussians;
-  const int grp = threadIdx.x / kReduceLanes, q = threadIdx.x % kReduceLanes;
-  const int shift = (threadIdx.x % 64) / kReduceLanes * kReduceLanes;  // the group's first lane in its wave
+  const int nb = int(min<int64_t>(kReduceGaussians, A.n - i0));
 
   // The chain rule's own inputs (thread t < 64 serves Gaussian i0 + t), read
   // now so that their latency overlaps the row sums.
   float cq[4] = {1.0f, 0.0f, 0.0f, 0.0f}, cls[3] = {0.0f, 0.0f, 0.0f}, clg = 0.0f;
   uint32_t ctc = 0;
-  if (int64_t(threadIdx.x) < min<int64_t>(kReduceGaussians, A.n - i0)) {
+  if (int(threadIdx.x) < nb) {
     const int64_t ic = i0 + threadIdx.x;
 #pragma unroll
     for (int k = 0; k < 4; ++k) cq[k] = A.quats[4 * ic + k];
@@ -815,83 +1002,16 @@ __global__ __launch_bounds__(kReduceBlock) void reduce_chain_kernel(BackwardArgs
     clg = A.logits[ic];
     ctc = A.tile_count[ic];
   }
-  // the row ranges of this group's Gaussians, loaded together up front
-  constexpr int kPer = (kReduceGaussians + GROUPS - 1) / GROUPS;
-  uint32_t tcs[kPer];
-  int64_t offs[kPer];
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int64_t i = i0 + grp + int64_t(k) * GROUPS;
-    const bool live = grp + k * GROUPS < kReduceGaussians && i < A.n;
-    tcs[k] = live ? A.tile_count[i] : 0u;
-    offs[k] = (ROWS && live) ? A.pair_offset[i] : 0;
+  if constexpr (ROWS) {
+    sum_rows<AS>(A, i0, nb, s_acc);
+  } else {
+    // the atomic modes' accumulators (zeroed before the backward), coalesced
+    for (int e = threadIdx.x; e < kReduceGaussians * NQ; e += kReduceBlock)
+      reinterpret_cast<float4*>(&s_acc[0][0])[e] =
+          e < nb * NQ ? reinterpret_cast<const float4*>(A.acc)[i0 * NQ + e] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    __syncthreads();
   }
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int gl = grp + k * GROUPS;
-    if (gl >= kReduceGaussians) break;
-    const int64_t i = i0 + gl;
-    const bool live = i < A.n;
-    const uint32_t tc = tcs[k];
-    float4 a[NC];
-#pragma unroll
-    for (int c = 0; c < NC; ++c) a[c] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if constexpr (ROWS) {
-      const float4* rows = reinterpret_cast<const float4*>(A.rows);
-      const int64_t r0 = offs[k] * A.rows_per_pair, r1 = r0 + int64_t(tc) * A.rows_per_pair;
-      for (int64_t rb = r0; rb < r1; rb += kFlagStep) {
-        // lane q reads flags q, q + L, q + 2L, ... of the step; bit f of m is
-        // row rb + f
-        uint32_t m = 0;
-#pragma unroll
-        for (int t = 0; t < kFlagStep / kReduceLanes; ++t) {
-          const int64_t rq = rb + q + t * kReduceLanes;
-          const bool act = rq < r1 && A.row_flag[rq] != 0;
-          const uint32_t b = uint32_t(__ballot(act) >> shift) & ((1u << kReduceLanes) - 1u);
-          m |= b << (t * kReduceLanes);
-        }
-        while (m) {
-          int k[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            k[u] = m ? __ffs(m) - 1 : -1;
-            m &= m ? m - 1 : 0u;
-          }
-          float4 v[4][NC];
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int c = 0; c < NC; ++c) {
-              const int col = q + c * kReduceLanes;
-              v[u][c] = (k[u] >= 0 && col < NQ) ? rows[(rb + k[u]) * NQ + col] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            }
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int c = 0; c < NC; ++c) {
-              a[c].x += v[u][c].x;
-              a[c].y += v[u][c].y;
-              a[c].z += v[u][c].z;
-              a[c].w += v[u][c].w;
-            }
-        }
-      }
-    } else if (live && tc) {
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const int col = q + c * kReduceLanes;
-        if (col < NQ) a[c] = reinterpret_cast<const float4*>(A.acc)[i * NQ + col];
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const int col = q + c * kReduceLanes;
-      if (col < NQ) reinterpret_cast<float4*>(s_acc[gl])[col] = a[c];
-    }
-  }
-  __syncthreads();
 
-  const int nb = int(min<int64_t>(kReduceGaussians, A.n - i0));
   for (int e = threadIdx.x; e < nb * 3 * K; e += kReduceBlock) {
     const int gl = e / (3 * K), v = e % (3 * K);
     A.g_sh[(i0 + gl) * 3 * K + v] = s_acc[gl][10 + v];
