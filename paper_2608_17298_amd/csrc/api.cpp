@@ -136,6 +136,8 @@ CamParams make_cam(const gart_camera* c) {
   for (int k = 0; k < 3; ++k) p.o[k] = -(R[k] * t[0] + R[3 + k] * t[1] + R[6 + k] * t[2]);
   p.fx = c->fx;
   p.fy = c->fy;
+  p.ifx = 1.0 / p.fx;
+  p.ify = 1.0 / p.fy;
   p.cx = c->cx;
   p.cy = c->cy;
   for (int k = 0; k < 3; ++k) {

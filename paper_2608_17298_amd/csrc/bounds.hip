@@ -383,12 +383,13 @@ __global__ __launch_bounds__(256) void emit_pairs_kernel(TileMapArgs A) {
     const int tx = s_tile[k][0] + int(q - row * ntx), ty = s_tile[k][1] + int(row);
     const int64_t j = first + jr;
     // corners of the pixel-centre rectangle of rect cap tile, depths along
-    // the tile's axis c
+    // the tile's axis c (camera coordinates by the reciprocal focal lengths:
+    // within an ulp of the pixel rays' quotients, inside the margin below)
     const int32_t* rc = A.rect + 4 * (i0 + k);
-    const double ax[2] = {(double(max(rc[0], tx * ts)) + 0.5 - A.cam.cx) / A.cam.fx,
-                          (double(min(rc[2], tx * ts + ts - 1)) + 0.5 - A.cam.cx) / A.cam.fx};
-    const double by[2] = {(double(max(rc[1], ty * ts)) + 0.5 - A.cam.cy) / A.cam.fy,
-                          (double(min(rc[3], ty * ts + ts - 1)) + 0.5 - A.cam.cy) / A.cam.fy};
+    const double ax[2] = {(double(max(rc[0], tx * ts)) + 0.5 - A.cam.cx) * A.cam.ifx,
+                          (double(min(rc[2], tx * ts + ts - 1)) + 0.5 - A.cam.cx) * A.cam.ifx};
+    const double by[2] = {(double(max(rc[1], ty * ts)) + 0.5 - A.cam.cy) * A.cam.ify,
+                          (double(min(rc[3], ty * ts + ts - 1)) + 0.5 - A.cam.cy) * A.cam.ify};
     double cax[3];
     tile_axis(A.cam, tx, ty, ts, cax);
     const double* Q = s_q[k];

@@ -29,6 +29,7 @@ struct CamParams {
   double o[3];        // camera centre in world space, o = -R^T t
   double Rt[9];       // R^T row-major (camera -> world rotation)
   double fx, fy, cx, cy;
+  double ifx, ify;    // 1 / fx, 1 / fy (for bounds only; pixel rays divide)
   double V0[4], V1[4], V3[4];  // rows of the world -> pixel-clip matrix (X, Y, w)
   int32_t W, H;
 };
@@ -61,8 +62,8 @@ __device__ __forceinline__ void pixel_ray(const CamParams& c, int px, int py, do
 // pixel coordinates ((tx + 1/2) ts, (ty + 1/2) ts)).  The tile's list keys are
 // depths measured along c.
 __device__ __forceinline__ void tile_axis(const CamParams& cam, int tx, int ty, int ts, double c[3]) {
-  const double a = (double(tx * ts) + 0.5 * ts - cam.cx) / cam.fx;
-  const double b = (double(ty * ts) + 0.5 * ts - cam.cy) / cam.fy;
+  const double a = (double(tx * ts) + 0.5 * ts - cam.cx) * cam.ifx;
+  const double b = (double(ty * ts) + 0.5 * ts - cam.cy) * cam.ify;
   const double inv = 1.0 / sqrt(fma(a, a, fma(b, b, 1.0)));
   c[0] = a * inv;
   c[1] = b * inv;
