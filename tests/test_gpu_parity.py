@@ -66,10 +66,11 @@ def _scene(name):
         sc, _, _ = random_tiny_scene(np.random.default_rng(13), 400, 79, 61, 3, spread=1.0, ls_mu=-2.4,
                                      ls_sd=0.5, logit_mu=10.0, logit_sd=2.0, cam=rotated_camera(79, 61))
         return sc
-    if name == "large_sh3":  # large low-opacity footprints: a reduction block's rows span several
-        # flag chunks (up to 6.3k rows) and Gaussians straddle chunk and share boundaries
+    if name in ("large_sh3", "large_sh3_tile16"):  # large low-opacity footprints: a reduction block's
+        # rows span several flag chunks (up to 6.3k rows at 8x8 tiles; four rows per pair at 16x16)
+        # and Gaussians straddle chunk and share boundaries
         sc, _, _ = random_tiny_scene(np.random.default_rng(23), 160, 160, 120, 3, spread=0.6, ls_mu=-0.7,
-                                     ls_sd=0.3, logit_mu=-2.5, high_sd=0.1)
+                                     ls_sd=0.3, logit_mu=-2.5, high_sd=0.1, tile=16 if name.endswith("16") else 8)
         return sc
     if name == "nonfinite_sh3":  # NaN / inf parameters and zero-norm quaternions among ordinary Gaussians
         rng = np.random.default_rng(17)
@@ -116,7 +117,8 @@ def _case(name, mode="gather", tile=None):
 
 
 SCENES = ["tiny", "small", "small_reduced", "1m_reduced", "stress_reduced", "random_sh3", "random_sh1", "random_sh2",
-          "random_sh3_tile16", "rotated_sh3", "opaque_sh3", "large_sh3", "nonfinite_sh3"]
+          "random_sh3_tile16", "rotated_sh3", "opaque_sh3", "large_sh3", "large_sh3_tile16",
+          "nonfinite_sh3"]
 
 
 @pytest.mark.parametrize("name", SCENES)
