@@ -29,7 +29,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gart_oracle.cpp")
 _LIB_DIR = os.path.join(_HERE, "_build")
-_LIB = os.path.join(_LIB_DIR, "liboracle.so")
+# GART_ORACLE_LIB names another build of this source to load instead (the
+# mutation test loads copies with a planted mistake this way).
+_LIB = os.environ.get("GART_ORACLE_LIB") or os.path.join(_LIB_DIR, "liboracle.so")
 
 STATE_ACTIVE = 0
 STATE_CULLED_OPACITY = 1
