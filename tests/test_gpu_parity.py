@@ -410,8 +410,11 @@ def test_backward_rejects_other_lt_format():
     torch.cuda.synchronize()
 
 
-def test_gather_deterministic():
-    sc = _scene("random_sh3")
+@pytest.mark.parametrize("name", ["random_sh3", "large_sh3", "large_sh3_tile16"])
+def test_gather_deterministic(name):
+    """Two gathers give bit-identical gradients, also where the reduction
+    splits Gaussians over lane groups and flag chunks (large footprints)."""
+    sc = _scene(name)
     a = run_gpu(sc, mode="gather")
     b = run_gpu(sc, mode="gather")
     for k in GROUPS:
